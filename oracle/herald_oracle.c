@@ -1,0 +1,245 @@
+/*
+ * HERALD reference oracle: plain, slow, fp64 CPU implementation of the
+ * sparse block-dLLM decode hot path. TEST INFRASTRUCTURE ONLY: it is used by
+ * the tests, the smoke check and the CPU-baseline leg of the benchmark, and
+ * never by the product library. It shares no code with the GPU path.
+ *
+ * Every input element (fp32, bf16 or fp64) is first decoded exactly to fp64;
+ * all arithmetic is fp64 with libm exp/sqrt, written as the definitions read,
+ * with no blocking, fusion or reordering.
+ *
+ * What each function follows:
+ *   herald_oracle_budget   per-KV-head budget k from a fraction of the prefix
+ *                          length (sec. IV-B.4 defines k per KV head; the
+ *                          rounding rule is a reading, half-up).
+ *   herald_oracle_select   representative-query selection (sec. IV-A.2) with
+ *                          the mean of the block's queries as the
+ *                          representative, scores over every prefix entry,
+ *                          per-query-head softmax statistics (m_g, l_g) and
+ *                          the GQA importance vector
+ *                          s_hat_h[s] = sum_g exp(s[g,s]-m_g)/l_g followed by
+ *                          one top-k per KV head (sec. IV-B.4). Ties go to the
+ *                          lower index; the output is in ascending index order.
+ *   herald_oracle_gather   copy of the selected K/V rows into a dense pool
+ *                          (sec. IV-B.3, the gather of the selected entries).
+ *   herald_oracle_attn     B-query GQA attention of a block over a context
+ *                          (the sparse pool or the full prefix) plus the
+ *                          block's own KV, no mask: bidirectional inside the
+ *                          block, the context is all prefix (sec. II-A).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* element types of the raw input buffers */
+enum { OR_F32 = 0, OR_BF16 = 1, OR_F64 = 2 };
+
+/* Exact decode of one element to fp64. bf16 is the top half of an fp32. */
+static double load_elem(const void *p, int type, int64_t i) {
+  if (type == OR_F64) return ((const double *)p)[i];
+  if (type == OR_F32) return (double)((const float *)p)[i];
+  uint32_t bits = ((uint32_t)((const uint16_t *)p)[i]) << 16;
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return (double)f;
+}
+
+static size_t elem_size(int type) {
+  return type == OR_F64 ? 8 : (type == OR_F32 ? 4 : 2);
+}
+
+int64_t herald_oracle_budget(int64_t S, int64_t num, int64_t den) {
+  /* k = clamp(floor(S*num/den + 1/2), 1, S) evaluated exactly in integers */
+  if (S <= 0 || den <= 0 || num < 0) return 0;
+  int64_t k = (S * num + den / 2) / den;
+  if (k < 1) k = 1;
+  if (k > S) k = S;
+  return k;
+}
+
+typedef struct {
+  double key;
+  int64_t idx;
+} ranked;
+
+/* total order: larger importance first, lower index first on equal values */
+static int cmp_rank(const void *a, const void *b) {
+  const ranked *x = (const ranked *)a, *y = (const ranked *)b;
+  if (x->key > y->key) return -1;
+  if (x->key < y->key) return 1;
+  return (x->idx < y->idx) ? -1 : (x->idx > y->idx);
+}
+
+static int cmp_i32(const void *a, const void *b) {
+  int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+  return (x > y) - (x < y);
+}
+
+/*
+ * One sequence. q_sel [B][Hq][d]; K [Hkv][S][d] (row s of head h at
+ * (h*S + s)*d). Writes s_hat [Hkv][S] (if non-NULL), and idx [Hkv][k]
+ * (ascending). Query head hq belongs to KV head hq / (Hq/Hkv).
+ * Returns 0 on success, -1 on bad arguments or allocation failure.
+ */
+int herald_oracle_select(int B, int Hq, int Hkv, int d, int64_t S,
+                         const void *q_sel, int q_type, const void *K,
+                         int k_type, int64_t k, double *s_hat_out,
+                         double *m_out, double *l_out, int32_t *idx_out) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || S < 1 || k < 1 ||
+      k > S)
+    return -1;
+  const int G = Hq / Hkv;
+  const double scale = 1.0 / sqrt((double)d);
+  int fail = 0;
+
+#pragma omp parallel for schedule(dynamic) reduction(| : fail)
+  for (int h = 0; h < Hkv; ++h) {
+    double *qbar = (double *)malloc(sizeof(double) * (size_t)G * d);
+    double *z = (double *)malloc(sizeof(double) * (size_t)G * S);
+    double *m = (double *)malloc(sizeof(double) * G);
+    double *l = (double *)malloc(sizeof(double) * G);
+    ranked *r = (ranked *)malloc(sizeof(ranked) * (size_t)S);
+    if (!qbar || !z || !m || !l || !r) {
+      fail = 1;
+      free(qbar); free(z); free(m); free(l); free(r);
+      continue;
+    }
+    /* representative query: mean of the B block queries of each head */
+    for (int g = 0; g < G; ++g) {
+      const int hq = h * G + g;
+      for (int e = 0; e < d; ++e) {
+        double acc = 0.0;
+        for (int i = 0; i < B; ++i)
+          acc += load_elem(q_sel, q_type, ((int64_t)i * Hq + hq) * d + e);
+        qbar[g * d + e] = acc / (double)B;
+      }
+    }
+    /* raw scores s[g,s] = scale * <qbar_g, k_s> over every prefix entry */
+    for (int g = 0; g < G; ++g)
+      for (int64_t s = 0; s < S; ++s) {
+        double acc = 0.0;
+        for (int e = 0; e < d; ++e)
+          acc += qbar[g * d + e] *
+                 load_elem(K, k_type, ((int64_t)h * S + s) * d + e);
+        z[g * S + s] = acc * scale;
+      }
+    /* softmax statistics per query head */
+    for (int g = 0; g < G; ++g) {
+      double mx = -INFINITY;
+      for (int64_t s = 0; s < S; ++s)
+        if (z[g * S + s] > mx) mx = z[g * S + s];
+      double sum = 0.0;
+      for (int64_t s = 0; s < S; ++s) sum += exp(z[g * S + s] - mx);
+      m[g] = mx;
+      l[g] = sum;
+      if (m_out) m_out[h * G + g] = mx;
+      if (l_out) l_out[h * G + g] = sum;
+    }
+    /* GQA importance: sum over the group of softmax-normalised scores */
+    for (int64_t s = 0; s < S; ++s) {
+      double acc = 0.0;
+      for (int g = 0; g < G; ++g) acc += exp(z[g * S + s] - m[g]) / l[g];
+      r[s].key = acc;
+      r[s].idx = s;
+      if (s_hat_out) s_hat_out[(int64_t)h * S + s] = acc;
+    }
+    /* one top-k per KV head: the first k under (importance desc, index asc) */
+    qsort(r, (size_t)S, sizeof(ranked), cmp_rank);
+    int32_t *out = idx_out + (int64_t)h * k;
+    for (int64_t j = 0; j < k; ++j) out[j] = (int32_t)r[j].idx;
+    qsort(out, (size_t)k, sizeof(int32_t), cmp_i32);
+    free(qbar); free(z); free(m); free(l); free(r);
+  }
+  return fail ? -1 : 0;
+}
+
+/*
+ * Gather of one sequence: pool[h][j][:] = K[h][idx[h][j]][:] for j < k,
+ * a byte copy. K is [Hkv][S][d]; pool is [Hkv][cap][d], cap >= k.
+ */
+int herald_oracle_gather(int Hkv, int d, int64_t S, const void *K, int type,
+                         const int32_t *idx, int64_t k, int64_t cap,
+                         void *pool) {
+  if (Hkv < 1 || d < 1 || k < 0 || k > cap) return -1;
+  const size_t row = elem_size(type) * (size_t)d;
+  for (int h = 0; h < Hkv; ++h)
+    for (int64_t j = 0; j < k; ++j) {
+      int64_t s = idx[(int64_t)h * k + j];
+      if (s < 0 || s >= S) return -1;
+      memcpy((char *)pool + ((int64_t)h * cap + j) * row,
+             (const char *)K + ((int64_t)h * S + s) * row, row);
+    }
+  return 0;
+}
+
+/*
+ * Block attention of one sequence. q [B][Hq][d]; context keys/values
+ * ctx_k/ctx_v [Hkv][n_ctx][d] (row stride d, head stride ctx_stride_h rows);
+ * the block's own keys/values blk_k/blk_v [B][Hkv][d]. For every block row i
+ * and query head hq: keys are the n_ctx context rows of KV head hq/G followed
+ * by the B block rows of that head, p = softmax(scale * q . key), and
+ * out[i][hq] = sum_j p_j value_j. out is fp64 [B][Hq][d].
+ */
+int herald_oracle_attn(int B, int Hq, int Hkv, int d, int64_t n_ctx,
+                       int64_t ctx_stride_h, const void *q, int q_type,
+                       const void *ctx_k, const void *ctx_v, int kv_type,
+                       const void *blk_k, const void *blk_v, int blk_type,
+                       double *out) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || n_ctx < 0 ||
+      ctx_stride_h < n_ctx)
+    return -1;
+  const int G = Hq / Hkv;
+  const double scale = 1.0 / sqrt((double)d);
+  const int64_t nkeys = n_ctx + B;
+  int fail = 0;
+
+#pragma omp parallel for collapse(2) schedule(dynamic) reduction(| : fail)
+  for (int i = 0; i < B; ++i)
+    for (int hq = 0; hq < Hq; ++hq) {
+      const int h = hq / G;
+      double *logit = (double *)malloc(sizeof(double) * (size_t)nkeys);
+      double *qv = (double *)malloc(sizeof(double) * (size_t)d);
+      if (!logit || !qv) {
+        fail = 1;
+        free(logit); free(qv);
+        continue;
+      }
+      for (int e = 0; e < d; ++e)
+        qv[e] = load_elem(q, q_type, ((int64_t)i * Hq + hq) * d + e);
+      for (int64_t j = 0; j < nkeys; ++j) {
+        double acc = 0.0;
+        for (int e = 0; e < d; ++e) {
+          double kv =
+              j < n_ctx
+                  ? load_elem(ctx_k, kv_type, ((int64_t)h * ctx_stride_h + j) * d + e)
+                  : load_elem(blk_k, blk_type,
+                              ((j - n_ctx) * Hkv + h) * (int64_t)d + e);
+          acc += qv[e] * kv;
+        }
+        logit[j] = acc * scale;
+      }
+      double mx = -INFINITY;
+      for (int64_t j = 0; j < nkeys; ++j)
+        if (logit[j] > mx) mx = logit[j];
+      double den = 0.0;
+      for (int64_t j = 0; j < nkeys; ++j) den += exp(logit[j] - mx);
+      /* logit[] now holds the attention probabilities p_j */
+      for (int64_t j = 0; j < nkeys; ++j) logit[j] = exp(logit[j] - mx) / den;
+      for (int e = 0; e < d; ++e) {
+        double acc = 0.0;
+        for (int64_t j = 0; j < nkeys; ++j) {
+          double v =
+              j < n_ctx
+                  ? load_elem(ctx_v, kv_type, ((int64_t)h * ctx_stride_h + j) * d + e)
+                  : load_elem(blk_v, blk_type,
+                              ((j - n_ctx) * Hkv + h) * (int64_t)d + e);
+          acc += logit[j] * v;
+        }
+        out[((int64_t)i * Hq + hq) * d + e] = acc;
+      }
+      free(logit);
+      free(qv);
+    }
+  return fail ? -1 : 0;
+}
