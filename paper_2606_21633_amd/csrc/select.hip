@@ -1,0 +1,510 @@
+// Selection phase on gfx950: representative query, full-cache scoring, GQA
+// importance and per-KV-head top-k (sec. IV-A.2 and sec. IV-B.4 of the paper).
+//
+// Four launches per call, all on the caller's stream:
+//   repq   : qbar[b][h][e][g] = mean over the B block queries (fp64), and
+//            clears the first-level histogram.
+//   score  : one workgroup per (chunk of 1024 cached rows, KV head, sequence).
+//            Streams K once with coalesced 128-bit non-temporal loads, turns
+//            the tile around in LDS so that each lane owns one row, and forms
+//            the G raw scores of that row with fp64 FMAs whose qbar operand
+//            comes from scalar registers. Writes the scores z (fp64) and the
+//            chunk's softmax statistics (max, sum of exp).
+//   norm   : merges the chunk statistics into (m_g, l_g), forms the GQA
+//            importance s_hat = sum_g exp(z_g - m_g) / l_g (fp64), stores its
+//            bit pattern as a 64-bit ranking key, and histograms the key's
+//            exponent field.
+//   topk   : one workgroup per (KV head, sequence). MSB-first radix select on
+//            the 64-bit keys (exponent from the histogram, then 11-bit digits;
+//            once the boundary bucket fits, it is compacted into LDS), then an
+//            ordered emission pass that writes the selected indices ascending,
+//            taking equal keys lowest index first.
+// Identical scores give bit-identical importances (one shift m_g per head for
+// every row), so exact ties are decided by index, as the definition says.
+#include <math.h>
+
+#include "common.h"
+
+namespace herald {
+namespace {
+
+constexpr int kTopkThreads = 1024;
+constexpr int kCandCap = 8192;
+constexpr int kEmitPerThread = 8;
+
+// (m, l) <- softmax-statistics merge of (m, l) and (m2, l2).
+__device__ __forceinline__ void merge_ml(double &m, double &l, double m2, double l2) {
+  if (m2 == -INFINITY) return;
+  if (m == -INFINITY) { m = m2; l = l2; return; }
+  if (m2 > m) { l = l * exp(m - m2) + l2; m = m2; }
+  else { l += l2 * exp(m2 - m); }
+}
+
+// ---------------------------------------------------------------- repq
+template <int D, int G, bool BF16>
+__global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_sel,
+                                                   double *__restrict__ qbar,
+                                                   uint32_t *__restrict__ hist,
+                                                   int block, int Hq, int Hkv) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  for (int t = threadIdx.x; t < D * G; t += 256) {
+    const int e = t % D, g = t / D;
+    const int hq = h * G + g;
+    double acc = 0.0;
+    for (int i = 0; i < block; ++i) {
+      const int64_t off = (((int64_t)b * block + i) * Hq + hq) * D + e;
+      float x;
+      if (BF16)
+        x = __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(q_sel)[off] << 16);
+      else
+        x = reinterpret_cast<const float *>(q_sel)[off];
+      acc += (double)x;
+    }
+    qbar[(bh * D + e) * G + g] = acc / (double)block;
+  }
+  for (int t = threadIdx.x; t < kHistBins; t += 256) hist[bh * kHistBins + t] = 0u;
+}
+
+// ---------------------------------------------------------------- score
+template <int D, int G, bool BF16>
+__global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
+                                                       const double *__restrict__ qbar,
+                                                       double *__restrict__ zspill,
+                                                       double *__restrict__ part,
+                                                       int Hkv, int64_t S_pad,
+                                                       int nchunk, double scale) {
+  constexpr int ELT = BF16 ? 2 : 4;
+  constexpr int RB = D * ELT;         // bytes per cached row
+  constexpr int LPR = RB / 16;        // lanes per row in one 1 KiB load
+  constexpr int RPL = 64 / LPR;       // rows per 1 KiB load
+  constexpr int NLD = LPR;            // 1 KiB loads per 64-row tile
+  constexpr int NT = kScoreChunk / 256;
+  constexpr int LSTR = RB + 16;       // padded LDS row stride
+  constexpr int EPC = 16 / ELT;       // elements per 16-byte chunk
+  __shared__ __attribute__((aligned(16))) char lds[4 * 64 * LSTR];
+  __shared__ double red[4][G], red2[4][G];
+
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = kv_len(kv, b);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  char *my = lds + wave * 64 * LSTR;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const double *qb = qbar + bh * D * G;
+  const int lr = lane / LPR, lc = lane % LPR;
+
+  uint4 buf[NLD];
+  auto load_tile = [&](int t) {
+    const int64_t r0 = c0 + (int64_t)(t * 4 + wave) * 64;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int64_t s = r0 + i * RPL + lr;
+      if (s < S)
+        buf[i] = ldg16_nt(kv.k + kv_row(kv, b, h, s) * ELT + lc * 16);
+      else
+        buf[i] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+
+  // lane-local online softmax statistics over the rows this lane scores
+  double m_l[G], l_l[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) { m_l[g] = -INFINITY; l_l[g] = 0.0; }
+  load_tile(0);
+#pragma unroll 1
+  for (int t = 0; t < NT; ++t) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i)
+      *reinterpret_cast<uint4 *>(my + (i * RPL + lr) * LSTR + lc * 16) = buf[i];
+    __builtin_amdgcn_wave_barrier();
+    if (t + 1 < NT) load_tile(t + 1);
+    double acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = 0.0;
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      const uint4 c = *reinterpret_cast<const uint4 *>(my + lane * LSTR + j * 16);
+      // A uniform zero the compiler cannot see through keeps the qbar loads
+      // in scalar registers inside the loop instead of hoisting all of them.
+      int zero = 0;
+      asm volatile("" : "+s"(zero));
+      const double *qq = qb + zero + j * EPC * G;
+      const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (BF16) {
+          const double x0 = (double)bf16_lo(w[u]);
+          const double x1 = (double)bf16_hi(w[u]);
+#pragma unroll
+          for (int g = 0; g < G; ++g) acc[g] = fma(x0, qq[(2 * u) * G + g], acc[g]);
+#pragma unroll
+          for (int g = 0; g < G; ++g) acc[g] = fma(x1, qq[(2 * u + 1) * G + g], acc[g]);
+        } else {
+          const double x = (double)__uint_as_float(w[u]);
+#pragma unroll
+          for (int g = 0; g < G; ++g) acc[g] = fma(x, qq[u * G + g], acc[g]);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    const int64_t s = c0 + (int64_t)(t * 4 + wave) * 64 + lane;
+    if (s < S) {
+      double *dst = zspill + (bh * S_pad + s) * G;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const double z = acc[g] * scale;
+        dst[g] = z;
+        // one exp per score: exp(-|z - m|) either rescales the old sum or
+        // is the new term
+        const double dz = z - m_l[g];
+        const double e = exp(-fabs(dz));
+        const bool up = dz > 0.0;
+        l_l[g] = up ? fma(l_l[g], e, 1.0) : l_l[g] + e;
+        m_l[g] = up ? z : m_l[g];
+      }
+    }
+  }
+
+  // merge the lane statistics across the workgroup in a fixed order
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    double m = m_l[g], l = l_l[g];
+#pragma unroll
+    for (int off = 1; off <= 32; off <<= 1) {
+      const double m2 = __shfl_xor(m, off, 64);
+      const double l2 = __shfl_xor(l, off, 64);
+      if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
+      else merge_ml(m, l, m2, l2);
+    }
+    if (lane == 0) { red[wave][g] = m; red2[wave][g] = l; }
+  }
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int g = threadIdx.x;
+    double m = red[0][g], l = red2[0][g];
+    for (int w = 1; w < 4; ++w) merge_ml(m, l, red[w][g], red2[w][g]);
+    double *p = part + ((bh * nchunk + chunk) * G + g) * 2;
+    p[0] = m;
+    p[1] = l;
+  }
+}
+
+// ---------------------------------------------------------------- norm
+template <int G>
+__global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ lens,
+                                                   const double *__restrict__ zspill,
+                                                   const double *__restrict__ part,
+                                                   uint64_t *__restrict__ keys,
+                                                   uint32_t *__restrict__ hist, int Hkv,
+                                                   int64_t S_pad, int nchunk, int64_t max_len) {
+  __shared__ uint32_t sh_hist[kHistBins];
+  __shared__ double sm[G], sinv[G];
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S) return;
+  const int nch = (int)((S + kScoreChunk - 1) / kScoreChunk);
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int t = threadIdx.x; t < kHistBins; t += 256) sh_hist[t] = 0u;
+
+  // Every workgroup of this (b, h) merges the same partials in the same
+  // order, so all of them see bit-identical (m_g, l_g).
+  for (int g = wave; g < G; g += 4) {
+    double m = -INFINITY, l = 0.0;
+    for (int c = lane; c < nch; c += 64) {
+      const double *p = part + ((bh * nchunk + c) * G + g) * 2;
+      merge_ml(m, l, p[0], p[1]);
+    }
+#pragma unroll
+    for (int off = 1; off <= 32; off <<= 1) {
+      const double m2 = __shfl_xor(m, off, 64);
+      const double l2 = __shfl_xor(l, off, 64);
+      // merge in a fixed (lower lane first) order
+      if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
+      else merge_ml(m, l, m2, l2);
+    }
+    if (lane == 0) { sm[g] = m; sinv[g] = 1.0 / l; }
+  }
+  __syncthreads();
+  double m[G], inv[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) { m[g] = sm[g]; inv[g] = sinv[g]; }
+
+  for (int i = 0; i < kScoreChunk / 256; ++i) {
+    const int64_t s = c0 + i * 256 + threadIdx.x;
+    const bool valid = s < S;
+    uint64_t key = 0;
+    if (valid) {
+      const double *zz = zspill + (bh * S_pad + s) * G;
+      double acc = 0.0;
+#pragma unroll
+      for (int g = 0; g < G; ++g) acc += exp(zz[g] - m[g]) * inv[g];
+      key = (uint64_t)__double_as_longlong(acc);
+      keys[bh * S_pad + s] = key;
+    }
+    // wave-aggregated histogram update: few distinct exponents per wave
+    const uint32_t bin = (uint32_t)(key >> 52) & (kHistBins - 1);
+    uint64_t pending = __ballot(valid);
+    while (pending) {
+      const int leader = __ffsll((unsigned long long)pending) - 1;
+      const uint32_t lb = __shfl(bin, leader, 64);
+      const uint64_t same = __ballot(valid && bin == lb) & pending;
+      if (lane == leader) atomicAdd(&sh_hist[lb], (uint32_t)__popcll(same));
+      pending &= ~same;
+    }
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < kHistBins; t += 256)
+    if (sh_hist[t]) atomicAdd(&hist[bh * kHistBins + t], sh_hist[t]);
+}
+
+// ---------------------------------------------------------------- topk
+// Block-wide exclusive scan of one int per thread (1024 threads).
+__device__ __forceinline__ int block_excl_scan(int v, int *wsum, int *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kTopkThreads / 64; ++w) {
+    const int x = wsum[w];
+    before += (w < wave) ? x : 0;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + incl - v;
+}
+
+// Wave 0 finds the digit d with above(d) < r <= above(d) + cnt[d], where
+// above(d) counts keys in bins > d. Results go to shared memory.
+__device__ __forceinline__ void find_digit(const uint32_t *cnt, int nbins, int r,
+                                           int *s_digit, int *s_above, int *s_cnt) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int per = (nbins + 63) / 64;          // bins per lane, from the top
+    const int hi = nbins - per * lane;           // lane covers [hi - per, hi)
+    int mine = 0;
+    for (int i = 0; i < per; ++i) {
+      const int bin = hi - 1 - i;
+      if (bin >= 0) mine += (int)cnt[bin];
+    }
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += y;
+    }
+    const int before = incl - mine;
+    if (before < r && r <= incl) {
+      int acc = before;
+      for (int i = 0; i < per; ++i) {
+        const int bin = hi - 1 - i;
+        if (bin < 0) break;
+        const int c = (int)cnt[bin];
+        if (acc + c >= r) { *s_digit = bin; *s_above = acc; *s_cnt = c; break; }
+        acc += c;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(
+    const int32_t *__restrict__ lens, const int32_t *__restrict__ kps, int k_max,
+    const uint64_t *__restrict__ keys, const uint32_t *__restrict__ hist,
+    int32_t *__restrict__ idx_out, int Hkv, int64_t S_pad, int64_t max_len) {
+  __shared__ uint32_t cnt[kHistBins];
+  __shared__ uint64_t cand[kCandCap];
+  __shared__ int wsum[kTopkThreads / 64];
+  __shared__ int s_digit, s_above, s_cnt, s_ncand;
+
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int tid = threadIdx.x;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int k = clamp_k(kps[b], S, k_max);
+  int32_t *out = idx_out + bh * k_max;
+  const uint64_t *kb = keys + bh * S_pad;
+
+  if (k == 0 || k == S) {
+    for (int j = tid; j < k_max; j += kTopkThreads) out[j] = j < k ? j : -1;
+    return;
+  }
+
+  for (int i = tid; i < kHistBins; i += kTopkThreads) cnt[i] = hist[bh * kHistBins + i];
+  if (tid == 0) s_ncand = 0;
+  __syncthreads();
+  find_digit(cnt, kHistBins, k, &s_digit, &s_above, &s_cnt);
+  uint64_t P = (uint64_t)s_digit;
+  int r = k - s_above;
+  int c = s_cnt;
+  int L = 52;
+  bool in_lds = false;
+  int ncand = 0;
+
+  // compact the keys whose top (64 - L) bits equal P into LDS
+  auto compact = [&]() {
+    for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t s = base + (int64_t)u * kTopkThreads + tid;
+        const bool match = s < S && (kb[s] >> L) == P;
+        const uint64_t bal = __ballot(match);
+        int slot0 = 0;
+        const int lane = tid & 63;
+        if (lane == 0 && bal) slot0 = atomicAdd(&s_ncand, __popcll(bal));
+        slot0 = __shfl(slot0, 0, 64);
+        if (match) {
+          const int slot = slot0 + __popcll(bal & ((1ull << lane) - 1ull));
+          if (slot < kCandCap) cand[slot] = kb[s];
+        }
+      }
+    }
+    __syncthreads();
+    ncand = min(s_ncand, kCandCap);
+    in_lds = true;
+  };
+
+  if (c != r && c <= kCandCap) compact();
+  while (c != r && L > 0) {
+    const int nb = L < 11 ? L : 11;
+    const int L2 = L - nb;
+    const uint32_t mask = (1u << nb) - 1u;
+    for (int i = tid; i < (1 << nb); i += kTopkThreads) cnt[i] = 0u;
+    __syncthreads();
+    if (in_lds) {
+      for (int i = tid; i < ncand; i += kTopkThreads) {
+        const uint64_t key = cand[i];
+        if ((key >> L) == P) atomicAdd(&cnt[(uint32_t)(key >> L2) & mask], 1u);
+      }
+    } else {
+      for (int64_t s = tid; s < S; s += kTopkThreads) {
+        const uint64_t key = kb[s];
+        if ((key >> L) == P) atomicAdd(&cnt[(uint32_t)(key >> L2) & mask], 1u);
+      }
+    }
+    __syncthreads();
+    find_digit(cnt, 1 << nb, r, &s_digit, &s_above, &s_cnt);
+    r -= s_above;
+    P = (P << nb) | (uint64_t)s_digit;
+    c = s_cnt;
+    L = L2;
+    __syncthreads();
+    if (!in_lds && c != r && c <= kCandCap) compact();
+  }
+
+  // Ordered emission: keys above the boundary bucket always, bucket members
+  // (equal top bits; exact ties once L == 0) lowest index first, r of them.
+  int base_eq = 0, base_sel = 0;
+  for (int64_t t0 = 0; t0 < S; t0 += (int64_t)kTopkThreads * kEmitPerThread) {
+    const int64_t s0 = t0 + (int64_t)tid * kEmitPerThread;
+    bool gt[kEmitPerThread], eq[kEmitPerThread];
+    int n_eq = 0;
+#pragma unroll
+    for (int u = 0; u < kEmitPerThread; ++u) {
+      const int64_t s = s0 + u;
+      const bool valid = s < S;
+      const uint64_t hi = valid ? (kb[s] >> L) : 0;
+      gt[u] = valid && hi > P;
+      eq[u] = valid && hi == P;
+      n_eq += eq[u];
+    }
+    int tot_eq;
+    int rank = base_eq + block_excl_scan(n_eq, wsum, &tot_eq);
+    bool take[kEmitPerThread];
+    int n_take = 0;
+#pragma unroll
+    for (int u = 0; u < kEmitPerThread; ++u) {
+      take[u] = gt[u] || (eq[u] && rank < r);
+      rank += eq[u];
+      n_take += take[u];
+    }
+    int tot_take;
+    int pos = base_sel + block_excl_scan(n_take, wsum, &tot_take);
+#pragma unroll
+    for (int u = 0; u < kEmitPerThread; ++u)
+      if (take[u]) {
+        if (pos < k) out[pos] = (int32_t)(s0 + u);  // counts are exact; guard anyway
+        ++pos;
+      }
+    base_eq += tot_eq;
+    base_sel += tot_take;
+  }
+  for (int j = k + tid; j < k_max; j += kTopkThreads) out[j] = -1;
+}
+
+template <int D, int G, bool BF16>
+hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView &kv,
+                           int Hq, int Hkv, const int32_t *k_per_seq, int k_max,
+                           int32_t *idx_out, const SelectWs &ws, hipStream_t stream) {
+  const double scale = 1.0 / sqrt((double)D);
+  repq_kernel<D, G, BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist,
+                                                                 block, Hq, Hkv);
+  const dim3 grid(ws.nchunk, Hkv, batch);
+  score_kernel<D, G, BF16><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part, Hkv,
+                                                      ws.S_pad, ws.nchunk, scale);
+  norm_kernel<G><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist,
+                                           Hkv, ws.S_pad, ws.nchunk, kv.max_len);
+  topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
+      kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
+                       SelectWs *layout, char *base) {
+  const int G = Hq / Hkv;
+  const int nchunk = (int)((max_seq_len + kScoreChunk - 1) / kScoreChunk);
+  const int64_t S_pad = (int64_t)nchunk * kScoreChunk;
+  const size_t bh = (size_t)batch * Hkv;
+  size_t off = 0;
+  const size_t o_qbar = off; off = align256(off + bh * d * G * sizeof(double));
+  const size_t o_z = off;    off = align256(off + bh * S_pad * G * sizeof(double));
+  const size_t o_part = off; off = align256(off + bh * nchunk * G * 2 * sizeof(double));
+  const size_t o_keys = off; off = align256(off + bh * S_pad * sizeof(uint64_t));
+  const size_t o_hist = off; off = align256(off + bh * kHistBins * sizeof(uint32_t));
+  if (layout) {
+    layout->qbar = reinterpret_cast<double *>(base + o_qbar);
+    layout->espill = reinterpret_cast<double *>(base + o_z);
+    layout->part = reinterpret_cast<double *>(base + o_part);
+    layout->keys = reinterpret_cast<uint64_t *>(base + o_keys);
+    layout->hist = reinterpret_cast<uint32_t *>(base + o_hist);
+    layout->S_pad = S_pad;
+    layout->nchunk = nchunk;
+  }
+  return off;
+}
+
+hipError_t launch_select(const herald_heads &hd, int batch, int block, const void *q_sel,
+                         const KvView &kv, int64_t /*max_seq_len*/,
+                         const int32_t *k_per_seq, int k_max, int32_t *idx_out,
+                         const SelectWs &ws, hipStream_t stream) {
+  const int G = hd.num_q_heads / hd.num_kv_heads;
+  const bool bf = hd.dtype == HERALD_BF16;
+  const int Hq = hd.num_q_heads, Hkv = hd.num_kv_heads;
+#define HERALD_SEL(D_, G_)                                                              \
+  if (hd.head_dim == D_ && G == G_)                                                     \
+    return bf ? launch_select_t<D_, G_, true>(batch, block, q_sel, kv, Hq, Hkv,         \
+                                              k_per_seq, k_max, idx_out, ws, stream)   \
+              : launch_select_t<D_, G_, false>(batch, block, q_sel, kv, Hq, Hkv,        \
+                                               k_per_seq, k_max, idx_out, ws, stream);
+  HERALD_SEL(64, 1) HERALD_SEL(64, 2) HERALD_SEL(64, 4) HERALD_SEL(64, 8)
+  HERALD_SEL(128, 1) HERALD_SEL(128, 2) HERALD_SEL(128, 4) HERALD_SEL(128, 8)
+#undef HERALD_SEL
+  return hipErrorInvalidValue;
+}
+
+}  // namespace herald

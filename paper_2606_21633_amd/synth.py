@@ -6,11 +6,13 @@ so that the GPU library and the CPU oracle can both be fed from it.
 
 Recipe (stand-in for the paper's LongBench prompts and model activations):
 
-* Every tensor is i.i.d. N(0, 1) drawn from ``numpy.random.default_rng(seed)``
-  (PCG64) in float32, in this fixed order: selection queries, per-step block
-  queries, K cache, V cache, per-step block K, per-step block V, completed
-  block K/V, then the planting draws. Device-resident workloads too large for
-  host memory use a seeded ``torch.Generator`` on the device instead.
+* Every tensor is i.i.d. N(0, 1) in float32. The slice of each tensor that
+  belongs to sequence b (selection queries, per-step block queries, K cache,
+  V cache, per-step block K/V, completed block K/V, next-block selection
+  queries) and the planting draws of sequence b come from their own PCG64
+  stream ``numpy.random.default_rng([seed, tensor, b])``. Device-resident
+  workloads too large for host memory use a seeded ``torch.Generator`` on
+  the device instead.
 * Heavy hitters: for every (sequence, KV head) a random unit vector u (from
   N(0, I_d), normalised) is drawn. 3u is added to a random 5% of the cached
   keys (round half-up of 0.05 S positions, drawn without replacement from
@@ -120,83 +122,110 @@ def _to_dtype(x: np.ndarray, dtype: str):
     return t.view(torch.int16).numpy().view(np.uint16)
 
 
-def make_host(wl: Workload, seed: int | None = None) -> dict:
+_TAGS = dict(q_sel=0, q=1, k=2, v=3, blk_k=4, blk_v=5, done_k=6, done_v=7, q_next=8,
+             plant=9, lens=10, pages=11)
+
+
+def _child(seed: int, tag: str, b: int = 0) -> np.random.Generator:
+    """Independent PCG64 stream keyed by (seed, tensor, sequence)."""
+    return np.random.default_rng([seed, _TAGS[tag], b])
+
+
+def _plant_plan(wl: Workload, seed: int, i: int, S: int):
+    """Heavy-hitter draws of sequence i: per KV head a unit vector u and the
+    key positions that get +3u (positions 0..3 get +6u)."""
+    rng = _child(seed, "plant", i)
+    us, rows = [], []
+    for _ in range(wl.num_kv_heads):
+        u = _unit(rng, wl.head_dim)
+        if wl.planting == "spans":
+            pos = np.concatenate([np.arange(st, st + ln) for st, ln in _spans(rng, S)]
+                                 or [np.zeros(0, np.int64)])
+        elif S > 4:
+            n = _planted_count(S)
+            pos = rng.choice(S - 4, size=min(n, S - 4), replace=False) + 4
+        else:
+            pos = np.zeros(0, np.int64)
+        us.append(u)
+        rows.append(pos)
+    return np.stack(us), rows
+
+
+def make_host(wl: Workload, seed: int | None = None, threads: int = 8) -> dict:
     """Host (numpy) inputs for one layer of ``wl``.
 
-    Returns a dict with
+    Every tensor slice of sequence b is drawn from its own PCG64 stream keyed
+    by (seed, tensor, b), so the draws run on several threads and are still
+    reproducible. Returns a dict with
       seq_lens [b] int32,
       q_sel [b][B][Hq][d], q [T][b][B][Hq][d],
       k, v: contiguous [b][Hkv][S_max][d] (zero rows beyond each length), or,
-            for paged workloads, pages [n_pages][Hkv][P][d] and
+            for paged workloads, pages_k/pages_v [n_pages][Hkv][P][d] and
             page_table [b][max_pages] int32,
       blk_k, blk_v [T][b][B][Hkv][d], done_k, done_v [b][B][Hkv][d],
       q_next [b][B][Hq][d] (the following block's selection queries).
     Float arrays are float32, or uint16 holding bfloat16 bits.
     """
+    import concurrent.futures as cf
     seed = wl.seed if seed is None else seed
-    rng = np.random.default_rng(seed)
     b, B, T = wl.batch, wl.block, wl.steps
     Hq, Hkv, d, G = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group
-    lens = seq_lens(wl, rng)
+    lens = seq_lens(wl, _child(seed, "lens"))
     S_max = int(lens.max())
-    f32 = np.float32
-    q_sel = rng.standard_normal((b, B, Hq, d), dtype=f32)
-    q = rng.standard_normal((T, b, B, Hq, d), dtype=f32)
-    k = np.zeros((b, Hkv, S_max, d), f32)
-    v = np.zeros((b, Hkv, S_max, d), f32)
-    for i in range(b):
-        k[i, :, :lens[i]] = rng.standard_normal((Hkv, int(lens[i]), d), dtype=f32)
-    for i in range(b):
-        v[i, :, :lens[i]] = rng.standard_normal((Hkv, int(lens[i]), d), dtype=f32)
-    blk_k = rng.standard_normal((T, b, B, Hkv, d), dtype=f32)
-    blk_v = rng.standard_normal((T, b, B, Hkv, d), dtype=f32)
-    done_k = rng.standard_normal((b, B, Hkv, d), dtype=f32)
-    done_v = rng.standard_normal((b, B, Hkv, d), dtype=f32)
-    q_next = rng.standard_normal((b, B, Hq, d), dtype=f32)
-    for i in range(b):
-        S = int(lens[i])
-        for h in range(Hkv):
-            u = _unit(rng, d)
-            if wl.planting == "spans":
-                for st, ln in _spans(rng, S):
-                    k[i, h, st:st + ln] += 3 * u
-            else:
-                n = _planted_count(S)
-                pos = rng.choice(S - 4, size=min(n, S - 4), replace=False) + 4
-                k[i, h, pos] += 3 * u
-            k[i, h, :min(4, S)] += 6 * u
-            hs = slice(h * G, (h + 1) * G)
-            q_sel[i, :, hs] += 3 * u
-            q[:, i, :, hs] += 3 * u
-            q_next[i, :, hs] += 3 * u
-    out = dict(seq_lens=lens)
-    for name, arr in (("q_sel", q_sel), ("q", q), ("blk_k", blk_k), ("blk_v", blk_v),
-                      ("done_k", done_k), ("done_v", done_v), ("q_next", q_next)):
-        out[name] = _to_dtype(arr, wl.dtype)
-    if wl.page_size > 0:
-        P = wl.page_size
+    et = np.float32 if wl.dtype == "f32" else np.uint16
+    plans = [_plant_plan(wl, seed, i, int(lens[i])) for i in range(b)]
+    out = dict(seq_lens=lens,
+               q_sel=np.empty((b, B, Hq, d), et), q=np.empty((T, b, B, Hq, d), et),
+               blk_k=np.empty((T, b, B, Hkv, d), et), blk_v=np.empty((T, b, B, Hkv, d), et),
+               done_k=np.empty((b, B, Hkv, d), et), done_v=np.empty((b, B, Hkv, d), et),
+               q_next=np.empty((b, B, Hq, d), et))
+    P = wl.page_size
+    if P > 0:
         npg = [(int(s) + P - 1) // P for s in lens]
         total = int(sum(npg))
-        perm = rng.permutation(total).astype(np.int32)
-        max_pages = max(npg)
-        table = np.zeros((b, max_pages), np.int32)
-        pk = np.zeros((total, Hkv, P, d), f32)
-        pv = np.zeros((total, Hkv, P, d), f32)
-        cursor = 0
+        perm = _child(seed, "pages").permutation(total).astype(np.int32)
+        table = np.zeros((b, max(npg)), np.int32)
+        starts = np.concatenate([[0], np.cumsum(npg)])
         for i in range(b):
-            for p in range(npg[i]):
-                phys = int(perm[cursor]); cursor += 1
-                table[i, p] = phys
-                s0, s1 = p * P, min((p + 1) * P, int(lens[i]))
-                pk[phys, :, :s1 - s0] = k[i, :, s0:s1]
-                pv[phys, :, :s1 - s0] = v[i, :, s0:s1]
-        out["pages_k"] = _to_dtype(pk, wl.dtype)
-        out["pages_v"] = _to_dtype(pv, wl.dtype)
+            table[i, :npg[i]] = perm[starts[i]:starts[i + 1]]
+        out["pages_k"] = np.zeros((total, Hkv, P, d), et)
+        out["pages_v"] = np.zeros((total, Hkv, P, d), et)
         out["page_table"] = table
-        del k, v
     else:
-        out["k"] = _to_dtype(k, wl.dtype)
-        out["v"] = _to_dtype(v, wl.dtype)
+        out["k"] = np.zeros((b, Hkv, S_max, d), et)
+        out["v"] = np.zeros((b, Hkv, S_max, d), et)
+
+    def fill(task):
+        name, i = task
+        rng = _child(seed, name, i)
+        u, rows = plans[i]
+        S = int(lens[i])
+        if name in ("k", "v"):
+            x = rng.standard_normal((Hkv, S, d), dtype=np.float32)
+            if name == "k":
+                for h in range(Hkv):
+                    x[h, rows[h]] += 3 * u[h]
+                    x[h, :min(4, S)] += 6 * u[h]
+            x = _to_dtype(x, wl.dtype)
+            if P > 0:
+                pad = np.zeros((Hkv, npg[i] * P, d), et)
+                pad[:, :S] = x
+                pages = np.ascontiguousarray(pad.reshape(Hkv, npg[i], P, d).transpose(1, 0, 2, 3))
+                out["pages_" + name][table[i, :npg[i]]] = pages
+            else:
+                out[name][i, :, :S] = x
+            return
+        tgt = out[name]
+        sl = (slice(None), i) if name in ("q", "blk_k", "blk_v") else (i,)
+        x = rng.standard_normal(tgt[sl].shape, dtype=np.float32)
+        if name in ("q_sel", "q", "q_next"):
+            x += 3 * np.repeat(u, G, axis=0)          # [Hq][d], broadcast over rows
+        tgt[sl] = _to_dtype(x, wl.dtype)
+
+    names = ("q_sel", "q", "k", "v", "blk_k", "blk_v", "done_k", "done_v", "q_next")
+    tasks = [(n, i) for n in names for i in range(b)]
+    with cf.ThreadPoolExecutor(threads) as ex:
+        list(ex.map(fill, tasks))
     return out
 
 

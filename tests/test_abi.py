@@ -1,0 +1,159 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol
+that include/herald.h declares, and rejects bad arguments with the
+documented status codes before enqueuing anything (all calls below fail
+host-side validation, so no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2606_21633_amd import herald as H
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "herald.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(H.LIB_PATH),
+                                reason="libherald.so not built")
+
+FAKE = 0x10000  # 16-byte aligned, never dereferenced: validation fails first
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(herald_\w+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for fn in ("herald_select", "herald_gather", "herald_block_attn",
+               "herald_decode_block"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(H.LIB_PATH)
+    for fn in declared_functions():
+        assert hasattr(lib, fn), fn
+    assert set(declared_functions()) == set(H.EXPORTS)
+
+
+def test_status_strings():
+    for st in range(5):
+        assert H.lib().herald_status_string(st)
+
+
+@pytest.mark.parametrize("S,num,den", [(1, 1, 20), (9, 1, 20), (10, 1, 20), (4096, 1, 20),
+                                       (32768, 1, 20), (131072, 1, 20), (65536, 1, 20),
+                                       (12345, 7, 100), (100, 1, 1), (100, 3, 2),
+                                       (0, 1, 20), (5, 1, 0), (5, -1, 3)])
+def test_budget_agrees_with_oracle(S, num, den):
+    assert H.budget_tokens(S, num, den) == oracle.budget(S, num, den)
+
+
+def _kv(**kw):
+    kv = H.KV(k=FAKE, v=FAKE, stride_b=8 * 1024 * 128, stride_h=1024 * 128, stride_s=128,
+              page_table=None, page_size=0, max_pages=0, stride_page=0, seq_lens=FAKE,
+              max_seq_len=1024)
+    for a, b in kw.items():
+        setattr(kv, a, b)
+    return kv
+
+
+def _select(hd=None, batch=2, block=4, q=FAKE, kv=None, kps=FAKE, k_max=52, idx=FAKE,
+            ws=FAKE * 256, ws_bytes=None):
+    hd = hd or H.heads(32, 8, 128, "bf16")
+    kv = kv or _kv()
+    if ws_bytes is None:
+        ws_bytes = H.select_workspace(hd, batch, kv.max_seq_len) - 1  # one byte short
+    return H.lib().herald_select(ctypes.byref(hd), batch, block, q, ctypes.byref(kv), kps,
+                                 k_max, idx, ws, ws_bytes, None)
+
+
+def test_select_validation():
+    assert _select() == H.ERR_WORKSPACE                       # one byte short
+    assert _select(ws=None, ws_bytes=1 << 40) == H.ERR_WORKSPACE
+    assert _select(ws=FAKE + 16, ws_bytes=1 << 40) == H.ERR_WORKSPACE  # not 256-aligned
+    assert _select(q=None) == H.ERR_INVALID_ARG
+    assert _select(q=FAKE + 2) == H.ERR_INVALID_ARG            # misaligned rows
+    assert _select(kps=None) == H.ERR_INVALID_ARG
+    assert _select(idx=None) == H.ERR_INVALID_ARG
+    assert _select(batch=0) == H.ERR_INVALID_ARG
+    assert _select(block=0) == H.ERR_INVALID_ARG
+    assert _select(block=65) == H.ERR_UNSUPPORTED
+    assert _select(k_max=0) == H.ERR_INVALID_ARG
+    assert _select(k_max=1025) == H.ERR_INVALID_ARG            # k_max > max_seq_len
+    assert _select(hd=H.heads(32, 8, 96, "bf16")) == H.ERR_UNSUPPORTED
+    assert _select(hd=H.heads(30, 8, 128, "bf16")) == H.ERR_INVALID_ARG  # H_q % H_kv
+    assert _select(hd=H.heads(48, 3, 128, "bf16")) == H.ERR_UNSUPPORTED  # G = 16
+    assert _select(hd=H.Heads(32, 8, 128, 7)) == H.ERR_INVALID_ARG       # dtype
+    assert _select(kv=_kv(k=None)) == H.ERR_INVALID_ARG
+    assert _select(kv=_kv(seq_lens=None)) == H.ERR_INVALID_ARG
+    assert _select(kv=_kv(max_seq_len=0)) == H.ERR_INVALID_ARG
+    assert _select(kv=_kv(stride_s=100)) == H.ERR_INVALID_ARG            # < head_dim
+    assert _select(kv=_kv(stride_s=132)) == H.ERR_INVALID_ARG            # rows not 16B
+    assert _select(kv=_kv(page_table=FAKE, page_size=12, max_pages=100,
+                          stride_page=8 * 16 * 128)) == H.ERR_INVALID_ARG  # not 2^n
+    assert _select(kv=_kv(page_table=FAKE, page_size=16, max_pages=10,
+                          stride_page=8 * 16 * 128)) == H.ERR_INVALID_ARG  # too few pages
+
+
+def test_workspace_queries():
+    hd = H.heads(32, 8, 128, "bf16")
+    assert H.select_workspace(hd, 16, 32768) > 16 * 8 * 32768 * 8
+    assert H.select_workspace(hd, 0, 32768) == 0
+    assert H.select_workspace(H.heads(32, 8, 96, "bf16"), 1, 10) == 0
+    assert H.block_attn_workspace(hd, 16, 32, 1670) >= 256
+    assert H.block_attn_workspace(hd, 16, 0, 1670) == 0
+    assert H.decode_block_workspace(hd, 8, 32, 65536, 3277) > H.select_workspace(hd, 8, 65536)
+
+
+def test_gather_and_attn_validation():
+    hd = H.heads(32, 8, 128, "bf16")
+    kv = _kv()
+    pool = H.Pool(FAKE, FAKE, 8 * 100 * 128, 100 * 128, 128, 100)
+    L = H.lib()
+    st = L.herald_gather(ctypes.byref(hd), 2, ctypes.byref(kv), FAKE, FAKE, 101,
+                         ctypes.byref(pool), 0, None)
+    assert st == H.ERR_INVALID_ARG                  # k_max beyond pool capacity
+    st = L.herald_gather(ctypes.byref(hd), 2, ctypes.byref(kv), FAKE, FAKE, 50,
+                         ctypes.byref(pool), 51, None)
+    assert st == H.ERR_INVALID_ARG                  # dst_row0 + k_max > capacity
+    st = L.herald_gather(ctypes.byref(hd), 2, ctypes.byref(_kv(v=None)), FAKE, FAKE, 50,
+                         ctypes.byref(pool), 0, None)
+    assert st == H.ERR_INVALID_ARG                  # gather needs V
+    ctx = _kv(max_seq_len=100000)
+    need = H.block_attn_workspace(hd, 2, 32, 100000)
+    st = L.herald_block_attn(ctypes.byref(hd), 2, 32, FAKE, ctypes.byref(ctx), FAKE, FAKE,
+                             FAKE, FAKE * 256, need - 1, None)
+    assert need > 256 and st == H.ERR_WORKSPACE
+    st = L.herald_block_attn(ctypes.byref(hd), 2, 32, None, ctypes.byref(ctx), FAKE, FAKE,
+                             FAKE, FAKE * 256, need, None)
+    assert st == H.ERR_INVALID_ARG
+
+
+def test_decode_block_validation():
+    hd = H.heads(32, 8, 128, "bf16")
+    L = H.lib()
+    cache = H.Pool(FAKE, FAKE, 8 * 2048 * 128, 2048 * 128, 128, 2048)
+    pool = H.Pool(FAKE, FAKE, 8 * 200 * 128, 200 * 128, 128, 200)
+    lay = H.Layer(cache, pool, pool, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0)
+    arr = (H.Layer * 1)(lay)
+    args = lambda **kw: dict(dict(nl=1, batch=2, block=32, steps=4, seq=FAKE, maxs=2000,
+                                  na=FAKE, maxa=150, ni=FAKE, kn=FAKE, kmax=100, dense=0,
+                                  ws=FAKE * 256, wsb=1 << 40), **kw)
+
+    def call(a):
+        return L.herald_decode_block(ctypes.byref(hd), a["nl"], a["batch"], a["block"],
+                                     a["steps"], arr, a["seq"], a["maxs"], a["na"], a["maxa"],
+                                     a["ni"], a["kn"], a["kmax"], a["dense"], a["ws"],
+                                     a["wsb"], None, None)
+    assert call(args(maxs=2017)) == H.ERR_INVALID_ARG   # cache capacity < S + block
+    assert call(args(kmax=169)) == H.ERR_INVALID_ARG    # idle capacity < k_max + block
+    assert call(args(maxa=201)) == H.ERR_INVALID_ARG    # active capacity
+    assert call(args(steps=0)) == H.ERR_INVALID_ARG
+    assert call(args(kn=None)) == H.ERR_INVALID_ARG
+    assert call(args(wsb=10)) == H.ERR_WORKSPACE
+    assert call(args(ws=FAKE * 256 + 16)) == H.ERR_WORKSPACE

@@ -1,0 +1,131 @@
+"""GPU parity of herald_select against the fp64 oracle: selected indices must
+be identical (ascending, -1 padded), on seeded inputs that span several
+scoring chunks with ragged tails, contiguous and paged caches, every
+supported group size and head dim, budget edge cases and exact ties."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_21633_amd import synth
+from tests.gpu_util import (DEV, Staged, assert_same_selection, boundary_gap, budgets,
+                            seq_kv_host, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def check_select(wl, inp=None, kps_h=None, k_max=None, seqs=None):
+    inp = synth.make_host(wl) if inp is None else inp
+    st = Staged(wl, inp)
+    lens = inp["seq_lens"]
+    kps_h = budgets(lens, *wl.budget) if kps_h is None else np.asarray(kps_h, np.int32)
+    if k_max is None:
+        k_max = int(max(1, min(kps_h.max(), lens.max())))
+    got, _ = st.select(kps_h, k_max)
+    near, gaps = 0, []
+    for b in (range(wl.batch) if seqs is None else seqs):
+        S = int(lens[b])
+        k = int(min(max(kps_h[b], 0), S, k_max))
+        assert (got[b, :, k:] == -1).all()
+        if k == 0:
+            continue
+        kh, _ = seq_kv_host(inp, b)
+        idx_o, shat, _, _ = oracle.select(inp["q_sel"][b], kh, k)
+        for h in range(wl.num_kv_heads):
+            near += assert_same_selection(got[b, h, :k], idx_o[h], shat[h], k)
+            gaps.append(boundary_gap(shat[h], k))
+    print(f"[select] {wl.name}: near-ties={near} min rel gap={min(gaps) if gaps else None}")
+    return near
+
+
+SMALL = synth.Workload("small bf16 ragged", "bf16", 3, 8, 2, 128, 5000, 4, 1,
+                       seq_len_lo=700, seed=11)
+
+
+def test_select_tiny_fp32_workload():
+    assert check_select(synth.TINY_F32) == 0
+
+
+@pytest.mark.parametrize("G,d,dtype", [(1, 64, "bf16"), (2, 128, "bf16"), (4, 128, "bf16"),
+                                       (8, 64, "bf16"), (4, 64, "f32"), (2, 128, "f32")])
+def test_select_group_and_dims(G, d, dtype):
+    wl = SMALL.replace(name=f"G{G} d{d} {dtype}", num_q_heads=2 * G, dtype=dtype,
+                       head_dim=d, seed=20 + G + d)
+    assert check_select(wl) == 0
+
+
+def test_select_ragged_paged():
+    wl = SMALL.replace(name="paged ragged", batch=5, page_size=16, seq_len=3000,
+                       seq_len_lo=17, seed=31)
+    assert check_select(wl) == 0
+
+
+@pytest.mark.parametrize("kps,k_max", [([1, 1, 1], 1), ([0, 5, 2000], 2000),
+                                        ([10 ** 6, 3, 7], 4000), ([-3, 700, 699], 700),
+                                        ([5000, 5000, 5000], 5000)])
+def test_select_budget_edges(kps, k_max):
+    inp = synth.make_host(SMALL)
+    k_max = min(k_max, int(inp["seq_lens"].max()))
+    assert check_select(SMALL, inp, np.array(kps), k_max) == 0
+
+
+def test_select_single_row_and_tiny_sequences():
+    wl = SMALL.replace(name="tiny seqs", batch=4, seq_len=3, seq_len_lo=1, seed=5)
+    assert check_select(wl, kps_h=np.array([1, 1, 2, 3])) == 0
+
+
+def _tie_inputs(S=3000, d=128):
+    rng = np.random.default_rng(77)
+    wl = synth.Workload("ties", "bf16", 2, 4, 1, d, S, 4, 1, seed=77)
+    inp = synth.make_host(wl)
+    k = inp["k"]
+    # sequence 0: every key identical -> the lowest k indices
+    k[0, 0, :] = k[0, 0, 123]
+    # sequence 1: three distinct key rows repeated across every scoring chunk
+    rows = k[1, 0, [10, 20, 30]].copy()
+    k[1, 0, :] = rows[rng.integers(0, 3, S)]
+    return wl, inp
+
+
+@pytest.mark.parametrize("kk", [1, 7, 1023, 1024, 1500, 2999])
+def test_select_exact_ties_go_to_lower_index(kk):
+    wl, inp = _tie_inputs()
+    assert check_select(wl, inp, np.array([kk, kk]), kk) == 0
+    st = Staged(wl, inp)
+    got, _ = st.select(np.array([kk, kk], np.int32), kk)
+    np.testing.assert_array_equal(got[0, 0], np.arange(kk))
+
+
+@pytest.mark.parametrize("pos", [0, 3, 63, 64, 1023, 1024, 2047, 4095, 4096, 4999])
+def test_select_dominant_key_found_anywhere(pos):
+    wl = SMALL.replace(name="dominant", batch=1, seq_len=5000, seq_len_lo=0, seed=pos)
+    inp = synth.make_host(wl)
+    qbar = (inp["q_sel"][0].astype(np.uint32) << 16).view(np.float32).mean(0)[0]
+    row = (40 * qbar / np.linalg.norm(qbar)).astype(np.float32)
+    import torch as _t
+    inp["k"][0, 0, pos] = _t.from_numpy(row).to(_t.bfloat16).view(_t.int16).numpy().view(np.uint16)
+    st = Staged(wl, inp)
+    got, _ = st.select(np.array([1], np.int32), 1)
+    assert got[0, 0, 0] == pos
+    assert check_select(wl, inp, np.array([1]), 1) == 0
+
+
+def test_select_layer_32k_workload_full():
+    """All 16 sequences x 8 KV heads of the 8B-class 32K layer."""
+    assert check_select(synth.LAYER_32K) == 0
+
+
+def test_select_long_128k_workload_full():
+    """All 4 sequences x 8 KV heads at 131072 cached tokens (spans)."""
+    assert check_select(synth.LONG_128K) == 0
+
+
+def test_select_ragged_paged_workload_sampled():
+    """The 64-sequence ragged paged layer, computed on the GPU in one call;
+    12 sequences (shortest, longest and 10 seeded picks) checked by the oracle."""
+    wl = synth.RAGGED_PAGED
+    inp = synth.make_host(wl)
+    lens = inp["seq_lens"]
+    pick = set(np.random.default_rng(0).choice(wl.batch, 10, replace=False).tolist())
+    pick |= {int(np.argmin(lens)), int(np.argmax(lens))}
+    assert check_select(wl, inp, seqs=sorted(pick)) == 0
