@@ -60,6 +60,8 @@ def _load():
         build(force=True)
     lib = ctypes.CDLL(_LIB_PATH)
     i64, i32, p, d = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_double
+    lib.herald_oracle_threads.restype = i32
+    lib.herald_oracle_threads.argtypes = []
     lib.herald_oracle_budget.restype = i64
     lib.herald_oracle_budget.argtypes = [i64, i64, i64]
     lib.herald_oracle_select.restype = i32
@@ -97,6 +99,11 @@ def _as_np(x):
 
 def _ptr(a):
     return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return int(_load().herald_oracle_threads())
 
 
 def budget(S: int, num: int = 1, den: int = 20) -> int:

@@ -28,6 +28,7 @@
  *                          block, the context is all prefix (sec. II-A).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -48,6 +49,9 @@ static double load_elem(const void *p, int type, int64_t i) {
 static size_t elem_size(int type) {
   return type == OR_F64 ? 8 : (type == OR_F32 ? 4 : 2);
 }
+
+/* Threads the OpenMP loops below run on. */
+int herald_oracle_threads(void) { return omp_get_max_threads(); }
 
 int64_t herald_oracle_budget(int64_t S, int64_t num, int64_t den) {
   /* k = clamp(floor(S*num/den + 1/2), 1, S) evaluated exactly in integers */
