@@ -80,7 +80,8 @@ typedef struct {
  *       page_table[b*max_pages + s/page_size]*stride_page + h*stride_h
  *       + (s % page_size)*stride_s
  * of k (and of v). seq_lens[b] (device int32) is the number of valid rows of
- * sequence b; max_seq_len (host) must bound every seq_lens[b].
+ * sequence b; max_seq_len (host) bounds them (larger values are clamped to
+ * it). page_size must be a power of two >= 8 (HERALD_ERR_UNSUPPORTED below 8).
  */
 typedef struct {
   const void *k;

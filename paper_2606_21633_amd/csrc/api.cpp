@@ -45,6 +45,7 @@ herald_status check_kv(const herald_heads *h, const herald_kv *kv, bool need_v) 
   if (kv->page_table) {
     const int32_t ps = kv->page_size;
     if (ps < 1 || (ps & (ps - 1))) return HERALD_ERR_INVALID_ARG;
+    if (ps < 8) return HERALD_ERR_UNSUPPORTED;  // a 1 KiB load spans up to 8 rows
     if (kv->max_pages < (kv->max_seq_len + ps - 1) / ps) return HERALD_ERR_INVALID_ARG;
     if (!stride_ok(kv->stride_page, elt)) return HERALD_ERR_INVALID_ARG;
   } else if (!stride_ok(kv->stride_b, elt)) {

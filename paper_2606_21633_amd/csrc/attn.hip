@@ -33,32 +33,40 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Source address (bytes) of 16-byte chunk c of key `key` of (b, h):
-// context rows first, then the block's own rows.
-__device__ __forceinline__ const char *key_chunk(const KvView &ctx, const char *blk,
-                                                 const char *ctxbase, int b, int h,
-                                                 int64_t key, int64_t n_ctx, int block,
-                                                 int Hkv, int D, int c, int elt) {
-  if (key < n_ctx) return ctxbase + kv_row(ctx, b, h, key) * elt + c * 16;
-  const int64_t i = key - n_ctx;
-  return blk + ((((int64_t)b * block + i) * Hkv + h) * D) * elt + c * 16;
+// Byte offset of row `key` of (b, h) among context rows then block rows.
+// Callers clamp key into [0, n_ctx + block).
+__device__ __forceinline__ const char *row_ptr(const KvView &ctx, const char *ctxbase,
+                                               const char *blk, int b, int h, int64_t key,
+                                               int64_t n_ctx, int block, int Hkv, int D,
+                                               int elt) {
+  if (key < n_ctx) return ctxbase + kv_row(ctx, b, h, key) * elt;
+  return blk + ((((int64_t)b * block + (key - n_ctx)) * Hkv + h) * D) * elt;
+}
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};  // v_cvt_pk_bf16_f32, round to nearest even
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(
+__global__ __launch_bounds__(NW * 64, 2) void attn_bf16_kernel(
     const uint16_t *__restrict__ q, KvView ctx, const uint16_t *__restrict__ blk_k,
     const uint16_t *__restrict__ blk_v, uint16_t *__restrict__ out,
     float *__restrict__ part_o, float2 *__restrict__ part_ml, int block, int Hq, int Hkv,
     int G, int M, int n_mblk, int nsplit, int keys_per_split, float sl2) {
   constexpr int KT = kKeyTile;
-  constexpr int KSTR = D * 2 + 16;   // LDS bytes per K row
-  constexpr int VSTR = KT * 2 + 16;  // LDS bytes per V^T row (one d)
-  constexpr int NKS = D / 16;        // MFMA k-steps of Q K^T
+  constexpr int KSTR = D * 2 + 16;   // LDS bytes per K row (padded)
+  constexpr int VSTR = KT * 2 + 16;  // LDS bytes per V^T row (one d, padded)
+  constexpr int NKS = D / 16;        // MFMA k-steps of K Q^T
   constexpr int NDT = D / 32;        // 32-wide d tiles of O^T
   constexpr int NTH = NW * 64;
   constexpr int CPR = D / 8;         // 16-byte chunks per row
-  __shared__ __attribute__((aligned(16))) char Ks[KT * KSTR];
-  __shared__ __attribute__((aligned(16))) char Vt[D * VSTR];
+  constexpr int KLD = KT * CPR / NTH;        // K chunks per thread per tile
+  constexpr int VTASK = (KT / 4) * CPR;      // (4 keys, one chunk) V tasks per tile
+  constexpr int VLD = (VTASK + NTH - 1) / NTH;
+  __shared__ __attribute__((aligned(16))) char Ks[2][KT * KSTR];
+  __shared__ __attribute__((aligned(16))) char Vt[2][D * VSTR];
 
   const int split = blockIdx.x;
   const int h = blockIdx.y / n_mblk, mblk = blockIdx.y % n_mblk;
@@ -91,51 +99,76 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(
   const char *bk = reinterpret_cast<const char *>(blk_k);
   const char *bv = reinterpret_cast<const char *>(blk_v);
 
+  // ---- global -> registers for one tile (keys past the end re-read the last
+  // valid row; their scores are masked) -------------------------------------
+  uint4 kreg[KLD];
+  uint4 vreg[VLD][4];
+  auto fetch = [&](int64_t t0) {
+#pragma unroll
+    for (int u = 0; u < KLD; ++u) {
+      const int x = tid + u * NTH;
+      const int kk = x / CPR, c = x % CPR;
+      const int64_t key = min(t0 + kk, k_end - 1);
+      kreg[u] = ldg16(row_ptr(ctx, ck, bk, b, h, key, n_ctx, block, Hkv, D, 2) + c * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < VLD; ++u) {
+      const int x = tid + u * NTH;
+      if (VTASK % NTH == 0 || x < VTASK) {
+        const int kg = x % (KT / 4), c = x / (KT / 4);
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const int64_t key = min(t0 + kg * 4 + a, k_end - 1);
+          vreg[u][a] = ldg16(row_ptr(ctx, cv, bv, b, h, key, n_ctx, block, Hkv, D, 2) + c * 16);
+        }
+      }
+    }
+  };
+  // ---- registers -> LDS: K row-major; V transposed, where inside each group
+  // of 16 keys key 8a + 4p + x sits at position 8p + 4a + x (the order in
+  // which the score registers feed the P^T operand) -------------------------
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < KLD; ++u) {
+      const int x = tid + u * NTH;
+      const int kk = x / CPR, c = x % CPR;
+      *reinterpret_cast<uint4 *>(Ks[buf] + kk * KSTR + c * 16) = kreg[u];
+    }
+#pragma unroll
+    for (int u = 0; u < VLD; ++u) {
+      const int x = tid + u * NTH;
+      if (VTASK % NTH == 0 || x < VTASK) {
+        const int kg = x % (KT / 4), c = x / (KT / 4);
+        const int kk0 = kg * 4;
+        const int pos0 = (kk0 & ~15) | (((kk0 >> 2) & 1) << 3) | (((kk0 >> 3) & 1) << 2);
+        const uint32_t w0[4] = {vreg[u][0].x, vreg[u][0].y, vreg[u][0].z, vreg[u][0].w};
+        const uint32_t w1[4] = {vreg[u][1].x, vreg[u][1].y, vreg[u][1].z, vreg[u][1].w};
+        const uint32_t w2[4] = {vreg[u][2].x, vreg[u][2].y, vreg[u][2].z, vreg[u][2].w};
+        const uint32_t w3[4] = {vreg[u][3].x, vreg[u][3].y, vreg[u][3].z, vreg[u][3].w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          // d = 8c + 2p (low halves) and 8c + 2p + 1 (high halves)
+          uint2 lo, hi;
+          lo.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x05040100u);
+          lo.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x05040100u);
+          hi.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x07060302u);
+          hi.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x07060302u);
+          *reinterpret_cast<uint2 *>(Vt[buf] + (8 * c + 2 * p) * VSTR + pos0 * 2) = lo;
+          *reinterpret_cast<uint2 *>(Vt[buf] + (8 * c + 2 * p + 1) * VSTR + pos0 * 2) = hi;
+        }
+      }
+    }
+  };
+
+  if (k_begin < k_end) {
+    fetch(k_begin);
+    stash(0);
+  }
+  __syncthreads();
+  int cur = 0;
   for (int64_t t0 = k_begin; t0 < k_end; t0 += KT) {
-    __syncthreads();
-    // K tile, row-major
-#pragma unroll
-    for (int u = tid; u < KT * CPR; u += NTH) {
-      const int kk = u / CPR, c = u % CPR;
-      const int64_t key = t0 + kk;
-      uint4 val = make_uint4(0u, 0u, 0u, 0u);
-      if (key < k_end)
-        val = ldg16(key_chunk(ctx, bk, ck, b, h, key, n_ctx, block, Hkv, D, c, 2));
-      *reinterpret_cast<uint4 *>(Ks + kk * KSTR + c * 16) = val;
-    }
-    // V tile, transposed: V^T[d][pos(key)], where inside each group of 16 keys
-    // key 8a + 4p + x sits at position 8p + 4a + x (the order in which the
-    // score registers feed the P^T operand).
-#pragma unroll
-    for (int u = tid; u < (KT / 4) * CPR; u += NTH) {
-      const int kg = u % (KT / 4), c = u / (KT / 4);
-      const int kk0 = kg * 4;
-      const int pos0 = (kk0 & ~15) | (((kk0 >> 2) & 1) << 3) | (((kk0 >> 3) & 1) << 2);
-      uint4 x[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int64_t key = t0 + kk0 + a;
-        x[a] = make_uint4(0u, 0u, 0u, 0u);
-        if (key < k_end)
-          x[a] = ldg16(key_chunk(ctx, bv, cv, b, h, key, n_ctx, block, Hkv, D, c, 2));
-      }
-      const uint32_t w0[4] = {x[0].x, x[0].y, x[0].z, x[0].w};
-      const uint32_t w1[4] = {x[1].x, x[1].y, x[1].z, x[1].w};
-      const uint32_t w2[4] = {x[2].x, x[2].y, x[2].z, x[2].w};
-      const uint32_t w3[4] = {x[3].x, x[3].y, x[3].z, x[3].w};
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        // d = 8c + 2p (low halves) and 8c + 2p + 1 (high halves)
-        uint2 lo, hi;
-        lo.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x05040100u);
-        lo.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x05040100u);
-        hi.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x07060302u);
-        hi.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x07060302u);
-        *reinterpret_cast<uint2 *>(Vt + (8 * c + 2 * p) * VSTR + pos0 * 2) = lo;
-        *reinterpret_cast<uint2 *>(Vt + (8 * c + 2 * p + 1) * VSTR + pos0 * 2) = hi;
-      }
-    }
-    __syncthreads();
+    const bool more = t0 + KT < k_end;
+    if (more) fetch(t0 + KT);  // in flight while this tile is computed
 
     // S^T (keys x queries) for the two 32-key halves of the tile
     f32x16 s[2];
@@ -145,23 +178,31 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(
       for (int j = 0; j < 16; ++j) s[t][j] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        const bf16x8 a = as_bf16x8(
-            *reinterpret_cast<const uint4 *>(Ks + (32 * t + l32) * KSTR + (8 * hh + 16 * ks) * 2));
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(
+            Ks[cur] + (32 * t + l32) * KSTR + (8 * hh + 16 * ks) * 2));
         s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[t], 0, 0, 0);
       }
     }
     // online softmax in the log2 domain; lane (l32, hh) holds keys
     // 32t + 8(j/4) + 4hh + j%4 of query column l32
-    float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int64_t key = t0 + 32 * t + 8 * (j >> 2) + 4 * hh + (j & 3);
-        const float x = key < k_end ? s[t][j] * sl2 : -INFINITY;
-        s[t][j] = x;
-        mx = fmaxf(mx, x);
-      }
+      for (int j = 0; j < 16; ++j) s[t][j] *= sl2;
+    if (t0 + KT > k_end) {  // last, partial tile
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int64_t key = t0 + 32 * t + 8 * (j >> 2) + 4 * hh + (j & 3);
+          if (key >= k_end) s[t][j] = -INFINITY;
+        }
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[t][j]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -177,28 +218,33 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(
     psum += __shfl_xor(psum, 32, 64);
     l_run = l_run * alpha + psum;
     m_run = m_new;
+    if (__ballot(alpha != 1.f)) {  // the running max moved for some row
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
+      for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) o[dt][j] *= alpha;
+        for (int j = 0; j < 16; ++j) o[dt][j] *= alpha;
+    }
 
     // O^T += V^T P^T, four 16-key steps
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int t = ks >> 1, base = (ks & 1) * 8;
       uint4 pw;
-      pw.x = pack_bf16x2(s[t][base + 0], s[t][base + 1]);
-      pw.y = pack_bf16x2(s[t][base + 2], s[t][base + 3]);
-      pw.z = pack_bf16x2(s[t][base + 4], s[t][base + 5]);
-      pw.w = pack_bf16x2(s[t][base + 6], s[t][base + 7]);
+      pw.x = pack2(s[t][base + 0], s[t][base + 1]);
+      pw.y = pack2(s[t][base + 2], s[t][base + 3]);
+      pw.z = pack2(s[t][base + 4], s[t][base + 5]);
+      pw.w = pack2(s[t][base + 6], s[t][base + 7]);
       const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x8 a = as_bf16x8(
-            *reinterpret_cast<const uint4 *>(Vt + (32 * dt + l32) * VSTR + (16 * ks + 8 * hh) * 2));
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(
+            Vt[cur] + (32 * dt + l32) * VSTR + (16 * ks + 8 * hh) * 2));
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[dt], 0, 0, 0);
       }
     }
+    if (more) stash(cur ^ 1);
+    __syncthreads();
+    cur ^= 1;
   }
 
   if (!rvalid) return;
@@ -211,8 +257,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(
 #pragma unroll
       for (int i4 = 0; i4 < 4; ++i4) {
         uint2 w;
-        w.x = pack_bf16x2(o[dt][4 * i4 + 0] * inv, o[dt][4 * i4 + 1] * inv);
-        w.y = pack_bf16x2(o[dt][4 * i4 + 2] * inv, o[dt][4 * i4 + 3] * inv);
+        w.x = pack2(o[dt][4 * i4 + 0] * inv, o[dt][4 * i4 + 1] * inv);
+        w.y = pack2(o[dt][4 * i4 + 2] * inv, o[dt][4 * i4 + 3] * inv);
         *reinterpret_cast<uint2 *>(orow + 32 * dt + 8 * i4 + 4 * hh) = w;
       }
   } else {
@@ -254,8 +300,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(
   const int g = r / block, i = r % block;
   uint16_t *orow = out + (((int64_t)b * block + i) * Hq + h * G + g) * D + d0;
   uint2 w;
-  w.x = pack_bf16x2(n0 * inv, n1 * inv);
-  w.y = pack_bf16x2(n2 * inv, n3 * inv);
+  w.x = pack2(n0 * inv, n1 * inv);
+  w.y = pack2(n2 * inv, n3 * inv);
   *reinterpret_cast<uint2 *>(orow) = w;
 }
 
@@ -286,7 +332,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     float logit = -INFINITY;
     if (key < n_keys) {
       const float *kr = reinterpret_cast<const float *>(
-          key_chunk(ctx, bk, ck, b, h, key, n_ctx, block, Hkv, D, 0, 4));
+          row_ptr(ctx, ck, bk, b, h, key, n_ctx, block, Hkv, D, 4));
       float acc = 0.f;
       for (int e = 0; e < D; ++e) acc = fmaf(q[qoff + e], kr[e], acc);
       logit = acc * scale;
@@ -306,7 +352,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     for (int jj = 0; jj < nvalid; ++jj) {
       const float pj = __shfl(p, jj, 64);
       const float *vr = reinterpret_cast<const float *>(
-          key_chunk(ctx, bv, cv, b, h, j0 + jj, n_ctx, block, Hkv, D, 0, 4));
+          row_ptr(ctx, cv, bv, b, h, j0 + jj, n_ctx, block, Hkv, D, 4));
 #pragma unroll
       for (int u = 0; u < ND; ++u) {
         const int d = lane + 64 * u;

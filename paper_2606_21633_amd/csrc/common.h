@@ -95,7 +95,7 @@ struct SelectWs {
   int nchunk;
 };
 
-constexpr int kScoreChunk = 1024;     // rows per scoring workgroup
+constexpr int kScoreChunk = 2048;     // rows per scoring workgroup
 constexpr int kHistBins = 2048;       // first-level radix bins (key >> 52)
 
 size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,

@@ -67,7 +67,7 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
 }
 
 // ---------------------------------------------------------------- score
-template <int D, int G, bool BF16>
+template <int D, int G, bool BF16, bool PAGED>
 __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
                                                        const double *__restrict__ qbar,
                                                        double *__restrict__ zspill,
@@ -94,17 +94,33 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
   const int64_t bh = (int64_t)b * Hkv + h;
   const double *qb = qbar + bh * D * G;
   const int lr = lane / LPR, lc = lane % LPR;
+  const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + lc * 16;
+
+  // Row s of this (b, h). In the paged layout the RPL rows of one load share
+  // a page (page_size is a multiple of RPL), so the page lookup is uniform.
+  auto row_addr = [&](int64_t s_base, int64_t s) -> const char * {
+    if (PAGED) {
+      const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s_base >> kv.page_shift)];
+      return kv.k + (page * kv.sp + (int64_t)h * kv.sh +
+                     (s & ((1 << kv.page_shift) - 1)) * kv.ss) * ELT + lc * 16;
+    }
+    return kbase + s * kv.ss * ELT;
+  };
 
   uint4 buf[NLD];
   auto load_tile = [&](int t) {
     const int64_t r0 = c0 + (int64_t)(t * 4 + wave) * 64;
+    if (r0 + 64 <= S) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int64_t s = r0 + i * RPL + lr;
-      if (s < S)
-        buf[i] = ldg16_nt(kv.k + kv_row(kv, b, h, s) * ELT + lc * 16);
-      else
+      for (int i = 0; i < NLD; ++i)
+        buf[i] = ldg16_nt(row_addr(r0 + i * RPL, r0 + i * RPL + lr));
+    } else {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const int64_t s = r0 + i * RPL + lr;
         buf[i] = make_uint4(0u, 0u, 0u, 0u);
+        if (s < S) buf[i] = ldg16_nt(row_addr(r0 + i * RPL, s));
+      }
     }
   };
 
@@ -115,22 +131,24 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
   load_tile(0);
 #pragma unroll 1
   for (int t = 0; t < NT; ++t) {
+    if (c0 + (int64_t)(t * 4) * 64 >= S) break;  // uniform: rest of chunk is empty
 #pragma unroll
     for (int i = 0; i < NLD; ++i)
       *reinterpret_cast<uint4 *>(my + (i * RPL + lr) * LSTR + lc * 16) = buf[i];
     __builtin_amdgcn_wave_barrier();
     if (t + 1 < NT) load_tile(t + 1);
+    // A uniform zero the compiler cannot see through keeps the qbar loads
+    // in scalar registers, issued per tile rather than hoisted out of it.
+    int zero = 0;
+    asm volatile("" : "+s"(zero));
+    const double *qt = qb + zero;
     double acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.0;
 #pragma unroll
     for (int j = 0; j < NLD; ++j) {
       const uint4 c = *reinterpret_cast<const uint4 *>(my + lane * LSTR + j * 16);
-      // A uniform zero the compiler cannot see through keeps the qbar loads
-      // in scalar registers inside the loop instead of hoisting all of them.
-      int zero = 0;
-      asm volatile("" : "+s"(zero));
-      const double *qq = qb + zero + j * EPC * G;
+      const double *qq = qt + j * EPC * G;
       const uint32_t w[4] = {c.x, c.y, c.z, c.w};
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -167,27 +185,32 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
     }
   }
 
-  // merge the lane statistics across the workgroup in a fixed order
+  // chunk statistics: max over the workgroup, then the rescaled sums
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    double m = m_l[g], l = l_l[g];
+    double m = m_l[g];
 #pragma unroll
-    for (int off = 1; off <= 32; off <<= 1) {
-      const double m2 = __shfl_xor(m, off, 64);
-      const double l2 = __shfl_xor(l, off, 64);
-      if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
-      else merge_ml(m, l, m2, l2);
-    }
-    if (lane == 0) { red[wave][g] = m; red2[wave][g] = l; }
+    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
+    if (lane == 0) red[wave][g] = m;
+  }
+  __syncthreads();
+  double mc[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+    mc[g] = fmax(fmax(red[0][g], red[1][g]), fmax(red[2][g], red[3][g]));
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    double v = m_l[g] == -INFINITY ? 0.0 : l_l[g] * exp(m_l[g] - mc[g]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    if (lane == 0) red2[wave][g] = v;
   }
   __syncthreads();
   if (threadIdx.x < G) {
     const int g = threadIdx.x;
-    double m = red[0][g], l = red2[0][g];
-    for (int w = 1; w < 4; ++w) merge_ml(m, l, red[w][g], red2[w][g]);
     double *p = part + ((bh * nchunk + chunk) * G + g) * 2;
-    p[0] = m;
-    p[1] = l;
+    p[0] = mc[g];
+    p[1] = (red2[0][g] + red2[1][g]) + (red2[2][g] + red2[3][g]);
   }
 }
 
@@ -235,6 +258,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
 
   for (int i = 0; i < kScoreChunk / 256; ++i) {
     const int64_t s = c0 + i * 256 + threadIdx.x;
+    if (c0 + i * 256 >= S) break;  // uniform
     const bool valid = s < S;
     uint64_t key = 0;
     if (valid) {
@@ -451,8 +475,12 @@ hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView
   repq_kernel<D, G, BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist,
                                                                  block, Hq, Hkv);
   const dim3 grid(ws.nchunk, Hkv, batch);
-  score_kernel<D, G, BF16><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part, Hkv,
-                                                      ws.S_pad, ws.nchunk, scale);
+  if (kv.pt)
+    score_kernel<D, G, BF16, true><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
+                                                             Hkv, ws.S_pad, ws.nchunk, scale);
+  else
+    score_kernel<D, G, BF16, false><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
+                                                              Hkv, ws.S_pad, ws.nchunk, scale);
   norm_kernel<G><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist,
                                            Hkv, ws.S_pad, ws.nchunk, kv.max_len);
   topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
