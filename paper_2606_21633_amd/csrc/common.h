@@ -112,7 +112,9 @@ hipError_t launch_gather(const herald_heads &hd, int batch, const KvView &kv,
 
 struct AttnPlan {
   int M;          // G * block query rows per (b, h)
-  int nwaves;     // waves per workgroup (32 rows each)
+  int nwaves;     // waves per pipeline (16 query rows each)
+  int pipes;      // pipelines per workgroup (alternate key tiles)
+  int key_tile;   // keys per tile
   int n_mblk;     // row blocks per (b, h)
   int nsplit;     // key splits of this call
   int nsplit_cap; // bound on nsplit for any context up to this one (sizes the workspace)
