@@ -46,20 +46,32 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
                                                    double *__restrict__ qbar,
                                                    uint32_t *__restrict__ hist,
                                                    int block, int Hq, int Hkv) {
+  constexpr int U = 64;  // loads in flight per thread: every block row at once
   const int h = blockIdx.x, b = blockIdx.y;
   const int64_t bh = (int64_t)b * Hkv + h;
   for (int t = threadIdx.x; t < D * G; t += 256) {
     const int e = t % D, g = t / D;
     const int hq = h * G + g;
+    const int64_t base = ((int64_t)b * block * Hq + hq) * D + e;
+    const int64_t step = (int64_t)Hq * D;
     double acc = 0.0;
-    for (int i = 0; i < block; ++i) {
-      const int64_t off = (((int64_t)b * block + i) * Hq + hq) * D + e;
-      float x;
-      if (BF16)
-        x = __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(q_sel)[off] << 16);
-      else
-        x = reinterpret_cast<const float *>(q_sel)[off];
-      acc += (double)x;
+    for (int i0 = 0; i0 < block; i0 += U) {
+      float x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u;
+        x[u] = 0.f;
+        if (i < block) {
+          if (BF16)
+            x[u] = __uint_as_float(
+                (uint32_t)reinterpret_cast<const uint16_t *>(q_sel)[base + i * step] << 16);
+          else
+            x[u] = reinterpret_cast<const float *>(q_sel)[base + i * step];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i0 + u < block) acc += (double)x[u];  // block-row order
     }
     qbar[(bh * D + e) * G + g] = acc / (double)block;
   }
@@ -67,8 +79,14 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
 }
 
 // ---------------------------------------------------------------- score
+// Workgroup = 2 wave pairs. A pair scores one 64-row tile at a time: both
+// waves stage the tile (coalesced 1 KiB loads) into LDS, then each lane owns
+// one row and each wave of the pair forms the partial dot products of one
+// half of the head dimension with the qbar half it holds in scalar registers.
+// The halves are added in a fixed order (low half + high half); the online
+// softmax statistics of the G heads are split between the two waves.
 template <int D, int G, bool BF16, bool PAGED>
-__global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
+__global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
                                                        const double *__restrict__ qbar,
                                                        double *__restrict__ zspill,
                                                        double *__restrict__ part,
@@ -79,25 +97,34 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
   constexpr int LPR = RB / 16;        // lanes per row in one 1 KiB load
   constexpr int RPL = 64 / LPR;       // rows per 1 KiB load
   constexpr int NLD = LPR;            // 1 KiB loads per 64-row tile
-  constexpr int NT = kScoreChunk / 256;
+  constexpr int NLDW = NLD / 2;       // loads per wave of the pair
   constexpr int LSTR = RB + 16;       // padded LDS row stride
   constexpr int EPC = 16 / ELT;       // elements per 16-byte chunk
-  __shared__ __attribute__((aligned(16))) char lds[4 * 64 * LSTR];
-  __shared__ double red[4][G], red2[4][G];
+  constexpr int HB = RB / 2;          // bytes of one half row
+  constexpr int NCH = HB / 16;        // 16-byte chunks per half row
+  constexpr int GH = G > 1 ? G / 2 : 1;  // heads whose statistics a wave keeps
+  constexpr int NTP = kScoreChunk / 128; // tiles per pair
+  __shared__ __attribute__((aligned(16))) char lds[2 * 64 * LSTR];
+  __shared__ double xch[2][2][64][GH];   // [pair][from half][row][g]
+  __shared__ double red[4][GH], red2[4][GH];
 
   const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  char *my = lds + wave * 64 * LSTR;
+  // wave index made provably uniform, so that qbar addresses stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int pair = wave >> 1, half = wave & 1;
+  char *my = lds + pair * 64 * LSTR;
   const int64_t bh = (int64_t)b * Hkv + h;
-  const double *qb = qbar + bh * D * G;
+  // qbar layout [e][g]; this wave's half of the elements
+  const double *qb = qbar + bh * D * G + (size_t)half * (D / 2) * G;
   const int lr = lane / LPR, lc = lane % LPR;
   const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + lc * 16;
+  // heads whose statistics this wave keeps: [g0, g0 + GH)
+  const int g0 = G > 1 ? half * GH : 0;
+  const bool keeps = G > 1 || half == 0;
 
-  // Row s of this (b, h). In the paged layout the RPL rows of one load share
-  // a page (page_size is a multiple of RPL), so the page lookup is uniform.
   auto row_addr = [&](int64_t s_base, int64_t s) -> const char * {
     if (PAGED) {
       const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s_base >> kv.page_shift)];
@@ -106,17 +133,18 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
     }
     return kbase + s * kv.ss * ELT;
   };
+  auto tile_row0 = [&](int t) { return c0 + (int64_t)(2 * t + pair) * 64; };
 
-  uint4 buf[NLD];
+  uint4 buf[NLDW];
   auto load_tile = [&](int t) {
-    const int64_t r0 = c0 + (int64_t)(t * 4 + wave) * 64;
-    if (r0 + 64 <= S) {
+    const int64_t r0 = tile_row0(t) + half * (NLDW * RPL);
+    if (r0 + NLDW * RPL <= S) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i)
+      for (int i = 0; i < NLDW; ++i)
         buf[i] = ldg16_nt(row_addr(r0 + i * RPL, r0 + i * RPL + lr));
     } else {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) {
+      for (int i = 0; i < NLDW; ++i) {
         const int64_t s = r0 + i * RPL + lr;
         buf[i] = make_uint4(0u, 0u, 0u, 0u);
         if (s < S) buf[i] = ldg16_nt(row_addr(r0 + i * RPL, s));
@@ -124,31 +152,32 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
     }
   };
 
-  // lane-local online softmax statistics over the rows this lane scores
-  double m_l[G], l_l[G];
+  double m_l[GH], l_l[GH];
 #pragma unroll
-  for (int g = 0; g < G; ++g) { m_l[g] = -INFINITY; l_l[g] = 0.0; }
+  for (int g = 0; g < GH; ++g) { m_l[g] = -INFINITY; l_l[g] = 0.0; }
   load_tile(0);
 #pragma unroll 1
-  for (int t = 0; t < NT; ++t) {
-    if (c0 + (int64_t)(t * 4) * 64 >= S) break;  // uniform: rest of chunk is empty
+  for (int t = 0; t < NTP; ++t) {
+    if (c0 + (int64_t)(2 * t) * 64 >= S) break;  // uniform: rest of chunk is empty
 #pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      *reinterpret_cast<uint4 *>(my + (i * RPL + lr) * LSTR + lc * 16) = buf[i];
-    __builtin_amdgcn_wave_barrier();
-    if (t + 1 < NT) load_tile(t + 1);
-    // A uniform zero the compiler cannot see through keeps the qbar loads
-    // in scalar registers, issued per tile rather than hoisted out of it.
-    int zero = 0;
-    asm volatile("" : "+s"(zero));
-    const double *qt = qb + zero;
+    for (int i = 0; i < NLDW; ++i)
+      *reinterpret_cast<uint4 *>(my + (half * NLDW * RPL + i * RPL + lr) * LSTR + lc * 16) =
+          buf[i];
+    __syncthreads();
+    if (t + 1 < NTP) load_tile(t + 1);
     double acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.0;
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const uint4 c = *reinterpret_cast<const uint4 *>(my + lane * LSTR + j * 16);
-      const double *qq = qt + j * EPC * G;
+    // two 16-byte chunks per step: enough to overlap the LDS and scalar
+    // loads, few enough that the fp64 operands fit in registers
+#pragma unroll 2
+    for (int j = 0; j < NCH; ++j) {
+      const uint4 c = *reinterpret_cast<const uint4 *>(my + lane * LSTR + half * HB + j * 16);
+      // A uniform zero the compiler cannot see through keeps the qbar loads
+      // in scalar registers, a chunk at a time, instead of hoisting them all.
+      int zero = 0;
+      asm volatile("" : "+s"(zero));
+      const double *qq = qb + zero + j * EPC * G;
       const uint32_t w[4] = {c.x, c.y, c.z, c.w};
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -166,51 +195,59 @@ __global__ __launch_bounds__(256, 2) void score_kernel(KvView kv,
         }
       }
     }
-    __builtin_amdgcn_wave_barrier();
-    const int64_t s = c0 + (int64_t)(t * 4 + wave) * 64 + lane;
-    if (s < S) {
+    // hand the partials of the other wave's heads over
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int owner = G > 1 ? g / GH : 0;
+      if (owner != half) xch[pair][half][lane][g % GH] = acc[g];
+    }
+    __syncthreads();
+    const int64_t s = tile_row0(t) + lane;
+    if (keeps && s < S) {
       double *dst = zspill + (bh * S_pad + s) * G;
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const double z = acc[g] * scale;
+      for (int gg = 0; gg < GH; ++gg) {
+        const int g = g0 + gg;
+        const double other = xch[pair][half ^ 1][lane][gg];
+        const double z = (half == 0 ? acc[g] + other : other + acc[g]) * scale;
         dst[g] = z;
         // one exp per score: exp(-|z - m|) either rescales the old sum or
         // is the new term
-        const double dz = z - m_l[g];
+        const double dz = z - m_l[gg];
         const double e = exp(-fabs(dz));
         const bool up = dz > 0.0;
-        l_l[g] = up ? fma(l_l[g], e, 1.0) : l_l[g] + e;
-        m_l[g] = up ? z : m_l[g];
+        l_l[gg] = up ? fma(l_l[gg], e, 1.0) : l_l[gg] + e;
+        m_l[gg] = up ? z : m_l[gg];
       }
     }
   }
 
-  // chunk statistics: max over the workgroup, then the rescaled sums
+  // chunk statistics: max over the workgroup, then the rescaled sums. Waves
+  // w and w ^ 2 (same half) keep the same heads.
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    double m = m_l[g];
+  for (int gg = 0; gg < GH; ++gg) {
+    double m = m_l[gg];
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
-    if (lane == 0) red[wave][g] = m;
+    if (lane == 0) red[wave][gg] = m;
   }
   __syncthreads();
-  double mc[G];
+  double mc[GH];
 #pragma unroll
-  for (int g = 0; g < G; ++g)
-    mc[g] = fmax(fmax(red[0][g], red[1][g]), fmax(red[2][g], red[3][g]));
+  for (int gg = 0; gg < GH; ++gg) mc[gg] = fmax(red[half][gg], red[half + 2][gg]);
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    double v = m_l[g] == -INFINITY ? 0.0 : l_l[g] * exp(m_l[g] - mc[g]);
+  for (int gg = 0; gg < GH; ++gg) {
+    double v = m_l[gg] == -INFINITY ? 0.0 : l_l[gg] * exp(m_l[gg] - mc[gg]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    if (lane == 0) red2[wave][g] = v;
+    if (lane == 0) red2[wave][gg] = v;
   }
   __syncthreads();
-  if (threadIdx.x < G) {
-    const int g = threadIdx.x;
+  if (wave < 2 && lane < GH && (G > 1 || wave == 0)) {
+    const int gg = lane, g = g0 + gg;
     double *p = part + ((bh * nchunk + chunk) * G + g) * 2;
-    p[0] = mc[g];
-    p[1] = (red2[0][g] + red2[1][g]) + (red2[2][g] + red2[3][g]);
+    p[0] = fmax(red[half][gg], red[half + 2][gg]);
+    p[1] = red2[half][gg] + red2[half + 2][gg];
   }
 }
 
@@ -379,10 +416,16 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   // compact the keys whose top (64 - L) bits equal P into LDS
   auto compact = [&]() {
     for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * 8) {
+      uint64_t key[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int64_t s = base + (int64_t)u * kTopkThreads + tid;
-        const bool match = s < S && (kb[s] >> L) == P;
+        key[u] = s < S ? kb[s] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t s = base + (int64_t)u * kTopkThreads + tid;
+        const bool match = s < S && (key[u] >> L) == P;
         const uint64_t bal = __ballot(match);
         int slot0 = 0;
         const int lane = tid & 63;
@@ -390,7 +433,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
         slot0 = __shfl(slot0, 0, 64);
         if (match) {
           const int slot = slot0 + __popcll(bal & ((1ull << lane) - 1ull));
-          if (slot < kCandCap) cand[slot] = kb[s];
+          if (slot < kCandCap) cand[slot] = key[u];
         }
       }
     }
@@ -412,9 +455,17 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
         if ((key >> L) == P) atomicAdd(&cnt[(uint32_t)(key >> L2) & mask], 1u);
       }
     } else {
-      for (int64_t s = tid; s < S; s += kTopkThreads) {
-        const uint64_t key = kb[s];
-        if ((key >> L) == P) atomicAdd(&cnt[(uint32_t)(key >> L2) & mask], 1u);
+      for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * 8) {
+        uint64_t key[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int64_t s = base + (int64_t)u * kTopkThreads + tid;
+          key[u] = s < S ? kb[s] : ~0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (base + (int64_t)u * kTopkThreads + tid < S && (key[u] >> L) == P)
+            atomicAdd(&cnt[(uint32_t)(key[u] >> L2) & mask], 1u);
       }
     }
     __syncthreads();
@@ -434,11 +485,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     const int64_t s0 = t0 + (int64_t)tid * kEmitPerThread;
     bool gt[kEmitPerThread], eq[kEmitPerThread];
     int n_eq = 0;
+    uint64_t key[kEmitPerThread];
+#pragma unroll
+    for (int u = 0; u < kEmitPerThread; ++u) key[u] = s0 + u < S ? kb[s0 + u] : 0;
 #pragma unroll
     for (int u = 0; u < kEmitPerThread; ++u) {
       const int64_t s = s0 + u;
       const bool valid = s < S;
-      const uint64_t hi = valid ? (kb[s] >> L) : 0;
+      const uint64_t hi = valid ? (key[u] >> L) : 0;
       gt[u] = valid && hi > P;
       eq[u] = valid && hi == P;
       n_eq += eq[u];
