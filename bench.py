@@ -50,6 +50,8 @@ def parse():
                     help="sequences in the CPU oracle sample (0: the whole batch)")
     ap.add_argument("--cpu-steps", type=int, default=0,
                     help="attention steps per sampled sequence (0: all T)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain copy of MIB MiB (counter calibration)")
     return ap.parse_args()
 
 
@@ -68,6 +70,8 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
     if args.workload == "ragged":
         return bench_ragged(args)
     if args.workload == "pipeline36":
@@ -157,7 +161,7 @@ def main():
     def timed(fn, reps, stream):
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        for _ in range(3):
+        for _ in range(min(3, reps)):
             fn()
         torch.cuda.synchronize()
         e0.record(stream)
@@ -176,10 +180,17 @@ def main():
     ws_att = H.workspace(H.block_attn_workspace(hd, b, B, max_ctx), dev)
     lens.copy_(lens0)
     torch.cuda.synchronize()
+    # the denoising phase alone: steps x T launches back to back on s_main,
+    # each step's own queries and block KV
+    n_att = args.steps * T
+
+    def denoise_phase():
+        for j in range(n_att):
+            t = j % T
+            H.block_attn(hd, b, B, q_steps[t], ctx_kv, blk_k[t], blk_v[t], out, ws_att,
+                         stream=s_main)
     with torch.cuda.stream(s_main):
-        ms_attn = timed(lambda: H.block_attn(hd, b, B, q_steps[0], ctx_kv, blk_k[0],
-                                             blk_v[0], out, ws_att, stream=s_main),
-                        args.reps, s_main)
+        ms_attn = timed(denoise_phase, 1, s_main) / n_att
         ms_sel = timed(lambda: H.select(hd, b, B, q_next, kv_cache, kps, k_max, idx, ws_sel,
                                         stream=s_main), max(5, args.reps // 3), s_main)
         ms_gat = timed(lambda: H.gather(hd, b, kv_cache, idx, kps, k_max,
@@ -222,8 +233,10 @@ def main():
         # the kernel is bound by HBM, and its MFMA rate is reported beside.
         "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "kernel": "herald_block_attn (attention + split "
-                     "combine)", "ms": round(ms_attn, 5), "bytes_per_launch": attn_bytes,
+                     "traffic": profiled_traffic(wl, args.dense),
+                     "kernel": "herald_block_attn (attention + split combine)",
+                     "ms": round(ms_attn, 5), "launches_timed": n_att,
+                     "bytes_per_launch": attn_bytes,
                      "flops_per_launch": attn_flops, "TFLOPs": round(attn_tflops, 2),
                      "mfma_frac": round(attn_tflops / peak, 4)},
         "selection": {"ms": round(ms_sel, 5), "k_bytes": sel_bytes,
@@ -241,6 +254,56 @@ def main():
         res["cpu_baseline"] = cpu_baseline(wl, inp, k_b, args.cpu_seqs or b,
                                            args.cpu_steps or T, args.dense)
     print(json.dumps(res), flush=True)
+
+
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_source_digest() -> str:
+    """sha256 of the attention kernel's source files (a traffic figure taken
+    from hardware counters holds only for the source it was measured on)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("attn.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2606_21633_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(wl, dense):
+    """HBM bytes per attention launch from the committed counter summary of
+    this workload (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy), or
+    None when there is none or the kernel source changed since."""
+    if dense or wl.name != "8B-layer bf16 16x(32q,8kv) d128 S32768 B32 T32":
+        return None
+    path = os.path.join(PROFILES, "block_attn_layer32k_traffic.txt")
+    try:
+        kv = {}
+        with open(path) as fh:
+            for line in fh:
+                if line.startswith("traffic:"):
+                    for tok in line.split()[1:]:
+                        k, _, v = tok.partition("=")
+                        kv[k] = v
+        if kv.get("source_sha256") != kernel_source_digest():
+            return None
+        return float(kv["bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int):
+    """A plain streaming copy of known size (dst = src * 1, fp32, 5 times) for
+    scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": True, "bytes_read_per_launch": n * 4,
+                      "bytes_written_per_launch": n * 4, "launches": 5}), flush=True)
 
 
 def _timed(fn, reps, stream):
