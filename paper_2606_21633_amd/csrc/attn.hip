@@ -26,7 +26,6 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 
-constexpr int kKeyTile = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
@@ -62,34 +61,62 @@ __device__ __forceinline__ float max4q(float v) {
   return fmaxf(__uint_as_float(c[0]), __uint_as_float(c[1]));
 }
 
-// One workgroup: P pipelines of NW waves. Each wave owns 16 query rows (the
-// MFMA N side of v_mfma_f32_16x16x32_bf16), each pipeline takes every P-th
-// key tile of the workgroup's key range, and the pipelines are merged in LDS
-// at the end. KT keys per tile: K row-major and V transposed in LDS, double
-// buffered per pipeline, one barrier per tile.
-template <int D, int NW, int P, int KT, bool PAGED>
-__global__ __launch_bounds__(NW * P * 64, 1) void attn_bf16_kernel(
+typedef short __attribute__((ext_vector_type(4))) s16x4;
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives element
+// i % 4 of the 8 bytes addressed by lanes 4s + i / 4, for s = 0..3.
+__device__ __forceinline__ uint2 lds_tr16(const char *p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4 *)(const __attribute__((address_space(3))) char *)p);
+  return __builtin_bit_cast(uint2, v);
+}
+// Workgroup barrier that leaves global loads in flight (the fence of
+// __syncthreads would wait for the register prefetch too); LDS writes are
+// complete before it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// LDS bytes of attn_bf16_kernel: the K/V ring (P pipelines x 2 stages of a
+// 32-key K and V tile), or the pipeline merge area if that is larger.
+template <int D, int RW, int NWP, int P>
+constexpr int attn_smem_bytes() {
+  constexpr int ring = P * 2 * 2 * 32 * (2 * D);
+  constexpr int slot = (RW / 16) * ((D / 16 + 1) * 4 + 1) + 1;
+  constexpr int merge = (P - 1) * NWP * 64 * slot * 4;
+  return ring > merge ? ring : merge;
+}
+
+// One workgroup = ROWS = NWP * RW query rows of one KV head over one key
+// split, as P pipelines of NWP waves. Pipeline p takes key tiles p, p + P, ...
+// (KT = 32 keys each) and the pipelines are merged in LDS at the end. Each
+// wave owns RW query rows: RW / 16 column blocks of v_mfma_f32_16x16x32_bf16
+// that share every K and V operand the wave reads from LDS.
+//
+// Tiles go global -> registers -> LDS. Two register sets per thread hold the
+// next two tiles of its pipeline while the current one is consumed from LDS
+// (two LDS stages per pipeline), so every load has about two rounds to land.
+// In LDS both K and V are row-major (2*D bytes per key) with the 16-byte
+// chunks of row r XOR-swizzled: K by fK(r) so that the ds_read_b128 of 16
+// rows in a quarter wave hit distinct banks, V by fV(r) so that the
+// transposed ds_read_b64_tr_b16 (8 rows x 32 bytes per half wave) do.
+template <int D, int RW, int NWP, int P, bool PAGED>
+__global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
     const uint16_t *__restrict__ q, KvView ctx, const uint16_t *__restrict__ blk_k,
     const uint16_t *__restrict__ blk_v, uint16_t *__restrict__ out,
     float *__restrict__ part_o, float2 *__restrict__ part_ml, int block, int Hq, int Hkv,
     int G, int M, int n_mblk, int nsplit, int keys_per_split, float sl2) {
-  constexpr int KSTR = D * 2 + 16;   // LDS bytes per K row (padded)
-  constexpr int VSTR = KT * 2 + 16;  // LDS bytes per V^T row (one d, padded)
-  constexpr int NKS = D / 32;        // k-steps of K Q^T (32 d each)
-  constexpr int NKB = KT / 16;       // 16-key blocks per tile
+  constexpr int KT = 32;             // keys per tile
+  constexpr int CB = RW / 16;        // column blocks (16 query rows) per wave
+  constexpr int NKS = D / 32;        // k-steps of K Q^T
   constexpr int NDB = D / 16;        // 16-d blocks of O^T
-  constexpr int NPS = KT / 32;       // k-steps of V^T P^T (32 keys each)
-  constexpr int NTH = NW * 64;       // threads per pipeline
+  constexpr int ROWB = 2 * D;        // bytes per K or V row
   constexpr int CPR = D / 8;         // 16-byte chunks per row
-  constexpr int KLD = KT * CPR / NTH;
-  // V is staged as tasks of TK consecutive keys x one 16-byte chunk; two-key
-  // tasks when four-key ones would leave threads of the pipeline idle
-  constexpr int TK = (KT / 4) * CPR >= NTH ? 4 : 2;
-  constexpr int VTASK = (KT / TK) * CPR;
-  constexpr int VLD = (VTASK + NTH - 1) / NTH;
-  constexpr int KBYTES = KT * KSTR, VBYTES = D * VSTR;
-  constexpr int STAGE = KBYTES + VBYTES;     // one buffer of one pipeline
-  static_assert(KLD * NTH == KT * CPR, "K tile must split evenly over a pipeline");
+  constexpr int RSH = D == 64 ? 1 : 0;  // log2(rows per 256 bytes)
+  constexpr int KB = KT * ROWB;      // bytes of one K (or V) tile
+  constexpr int STAGE = 2 * KB;
+  constexpr int NTH = NWP * 64;      // threads per pipeline
+  constexpr int LPT = KT * CPR / NTH;  // 16-byte chunks per thread per K (or V) tile
+  static_assert(LPT * NTH == KT * CPR, "tile must split evenly over a pipeline");
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
   // Workgroups are dealt round-robin to the 8 XCDs by linear id. When the row
@@ -111,286 +138,335 @@ __global__ __launch_bounds__(NW * P * 64, 1) void attn_bf16_kernel(
       h = pair % hk;
     }
   }
-  const int pipe = threadIdx.x / NTH;
-  const int tid = threadIdx.x % NTH, wave = tid >> 6, lane = tid & 63;
-  const int q4 = lane >> 4, l16 = lane & 15;
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int pipe = wv / NWP, w = wv % NWP;
+  const int tid = threadIdx.x % NTH, lane = threadIdx.x & 63, q4 = lane >> 4, l16 = lane & 15;
   const int64_t n_ctx = kv_len(ctx, b);
   const int64_t n_keys = n_ctx + block;
   const int64_t k_begin = (int64_t)split * keys_per_split;
   const int64_t k_end = min(k_begin + (int64_t)keys_per_split, n_keys);
-  char *my = smem + pipe * 2 * STAGE;
+  // The split's keys are tiled in two runs: context rows [c_lo, c_hi) and the
+  // block's own rows [r_lo, r_hi) (block row indices); every tile then has a
+  // uniform base, a uniform row stride and a count of valid rows.
+  const int64_t c_lo = k_begin, c_hi = min(k_end, n_ctx);
+  const int ntc = c_hi > c_lo ? (int)((c_hi - c_lo + KT - 1) / KT) : 0;
+  const int64_t r_lo = max(k_begin, n_ctx) - n_ctx, r_hi = k_end - n_ctx;
+  const int ntb = r_hi > r_lo ? (int)((r_hi - r_lo + KT - 1) / KT) : 0;
+  const int ntile = ntc + ntb;
+  const int rounds = (ntile + P - 1) / P;
+  char *ring = smem + pipe * 2 * STAGE;
 
-  const int r = (mblk * NW + wave) * 16 + l16;  // query row of this lane's column
-  const bool rvalid = r < M;
-  const int g = rvalid ? r / block : 0, i = rvalid ? r % block : 0;
-  const int64_t qoff = ((((int64_t)b * block + i) * Hq + h * G + g) * D);
-  bf16x8 qf[NKS];
+  // ---- query fragments (loaded first: their wait below leaves the tile
+  // prefetch issued after them in flight)
+  const int rbase = mblk * (NWP * RW) + w * RW;
+  bf16x8 qf[CB][NKS];
+  int64_t qoff[CB];
+  bool rvalid[CB];
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks)
-    qf[ks] = rvalid ? as_bf16x8(ldg16(q + qoff + 32 * ks + 8 * q4))
-                    : as_bf16x8(make_uint4(0u, 0u, 0u, 0u));
-  // o[NDB] accumulates the softmax denominator (a block of ones times P^T)
-  f32x4 o[NDB + 1];
+  for (int cb = 0; cb < CB; ++cb) {
+    const int r = rbase + 16 * cb + l16;
+    rvalid[cb] = r < M;
+    const int g = rvalid[cb] ? r / block : 0, i = rvalid[cb] ? r % block : 0;
+    qoff[cb] = (((int64_t)b * block + i) * Hq + h * G + g) * D;
 #pragma unroll
-  for (int db = 0; db <= NDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY;  // reference max of raw scores
-  const bf16x8 ones = as_bf16x8(make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u));
+    for (int ks = 0; ks < NKS; ++ks)
+      qf[cb][ks] = rvalid[cb] ? as_bf16x8(ldg16(q + qoff[cb] + 32 * ks + 8 * q4))
+                              : as_bf16x8(make_uint4(0u, 0u, 0u, 0u));
+  }
 
-  // Row `key` of (b, h): the first n_ctx keys are context rows, the next
-  // `block` keys the block's own rows. Contiguous contexts and the block rows
-  // are both linear in the key, so the address is a select, not a branch.
-  const char *bk = reinterpret_cast<const char *>(blk_k) +
-                   (((int64_t)b * block * Hkv + h) * D - n_ctx * Hkv * D) * 2;
-  const char *bv = reinterpret_cast<const char *>(blk_v) +
-                   (((int64_t)b * block * Hkv + h) * D - n_ctx * Hkv * D) * 2;
-  const int64_t brs = (int64_t)Hkv * D * 2;   // block row stride (bytes)
+  // ---- tile addressing: chunk u of this thread is row x / CPR, chunk x % CPR
+  // with x = tid + u * NTH, for K and V alike
   const int64_t crs = ctx.ss * 2;             // context row stride (bytes)
+  const int64_t brs = (int64_t)Hkv * D * 2;   // block row stride (bytes)
   const char *ckb = ctx.k + ((int64_t)b * ctx.sb + (int64_t)h * ctx.sh) * 2;
   const char *cvb = ctx.v + ((int64_t)b * ctx.sb + (int64_t)h * ctx.sh) * 2;
-  auto kaddr = [&](const char *cbase, const char *bbase, bool v, int64_t key) -> const char * {
-    key = min(key, k_end - 1);
-    if (PAGED && key < n_ctx) return (v ? ctx.v : ctx.k) + kv_row(ctx, b, h, key) * 2;
-    return key < n_ctx ? cbase + key * crs : bbase + key * brs;
+  const char *bkb = reinterpret_cast<const char *>(blk_k) + ((int64_t)b * block * Hkv + h) * D * 2;
+  const char *bvb = reinterpret_cast<const char *>(blk_v) + ((int64_t)b * block * Hkv + h) * D * 2;
+  // Tile `it` of this pipeline (tile index it * P + pipe): K and V bases, row
+  // stride and valid rows (0 past the split's last tile, whose rows are then
+  // read from the last tile, in bounds, and masked).
+  struct Tile {
+    const char *k, *v;
+    int64_t r0;       // first context row (context tiles)
+    int stride, nvalid;
+    bool in_ctx;
   };
-
-  uint4 kreg[KLD];
-  uint4 vreg[VLD][TK];
-  // per-thread byte offsets inside a tile of contiguous context rows
-  uint32_t koff[KLD], voff[VLD];
+  auto tile = [&](int it) {
+    int t = it * P + pipe;
+    const bool live = t < ntile;
+    t = live ? t : (ntile > 0 ? ntile - 1 : 0);
+    Tile d;
+    d.in_ctx = t < ntc;
+    if (t < ntc) {
+      const int64_t r0 = c_lo + (int64_t)t * KT;
+      d.r0 = r0;
+      d.k = ckb + r0 * crs;
+      d.v = cvb + r0 * crs;
+      d.stride = (int)crs;
+      d.nvalid = (int)min((int64_t)KT, c_hi - r0);
+    } else {
+      // (a split with no keys at all reads block row 0, masked)
+      const int64_t r0 = ntile > 0 ? r_lo + (int64_t)(t - ntc) * KT : 0;
+      d.r0 = 0;
+      d.k = bkb + r0 * brs;
+      d.v = bvb + r0 * brs;
+      d.stride = (int)brs;
+      d.nvalid = ntile > 0 ? (int)min((int64_t)KT, r_hi - r0) : 1;
+    }
+    d.nvalid = live ? d.nvalid : 0;
+    return d;
+  };
+  uint4 kr[2][LPT], vr[2][LPT];
+  auto fetch = [&](uint4 (&kx)[LPT], uint4 (&vx)[LPT], int it) {
+    const Tile d = tile(it);
+    const int last = d.nvalid > 0 ? d.nvalid - 1 : 0;
+    if (PAGED && d.in_ctx) {  // context rows through the page table
 #pragma unroll
-  for (int u = 0; u < KLD; ++u) {
-    const int x = tid + u * NTH;
-    koff[u] = (uint32_t)((x / CPR) * crs + (x % CPR) * 16);
-  }
-#pragma unroll
-  for (int u = 0; u < VLD; ++u) {
-    const int x = tid + u * NTH;
-    voff[u] = (uint32_t)(((x % (KT / TK)) * TK) * crs + (x / (KT / TK)) * 16);
-  }
-  // global -> registers for the tile at t0. A tile wholly inside a
-  // contiguous context is a uniform base plus the offsets above; otherwise
-  // keys past the end re-read the last valid row (their scores are masked).
-  auto fetch = [&](int64_t t0) {
-    if (!PAGED && t0 + KT <= n_ctx && t0 + KT <= k_end) {
-      const char *kt = ckb + t0 * crs, *vt = cvb + t0 * crs;
-#pragma unroll
-      for (int u = 0; u < KLD; ++u) kreg[u] = ldg16(kt + koff[u]);
-#pragma unroll
-      for (int u = 0; u < VLD; ++u) {
+      for (int u = 0; u < LPT; ++u) {
         const int x = tid + u * NTH;
-        if (VTASK % NTH == 0 || x < VTASK) {
-#pragma unroll
-          for (int a = 0; a < TK; ++a) vreg[u][a] = ldg16(vt + voff[u] + a * crs);
-        }
+        const int64_t e = kv_row(ctx, b, h, d.r0 + min(x / CPR, last)) * 2 + (x % CPR) * 16;
+        kx[u] = ldg16(ctx.k + e);
+        vx[u] = ldg16(ctx.v + e);
       }
       return;
     }
-    asm volatile("");  // keep this path a branch
 #pragma unroll
-    for (int u = 0; u < KLD; ++u) {
+    for (int u = 0; u < LPT; ++u) {
       const int x = tid + u * NTH;
-      const int kk = x / CPR, c = x % CPR;
-      kreg[u] = ldg16(kaddr(ckb, bk, false, t0 + kk) + c * 16);
-    }
-#pragma unroll
-    for (int u = 0; u < VLD; ++u) {
-      const int x = tid + u * NTH;
-      if (VTASK % NTH == 0 || x < VTASK) {
-        const int kg = x % (KT / TK), c = x / (KT / TK);
-#pragma unroll
-        for (int a = 0; a < TK; ++a)
-          vreg[u][a] = ldg16(kaddr(cvb, bv, true, t0 + kg * TK + a) + c * 16);
-      }
+      const uint32_t off = (uint32_t)(min(x / CPR, last) * d.stride + (x % CPR) * 16);
+      kx[u] = ldg16(d.k + off);
+      vx[u] = ldg16(d.v + off);
     }
   };
-  // registers -> LDS: K row-major; V transposed. Inside each group of 32 keys
-  // key 16a + 4q + x sits at position 8q + 4a + x: the order in which a lane's
-  // score registers feed the P^T operand of one 32-key k-step.
-  auto stash = [&](int buf) {
-    char *Ks = my + buf * STAGE, *Vt = Ks + KBYTES;
+  // registers -> LDS stage `stg` (swizzled row-major K and V)
+  auto stash = [&](const uint4 (&kx)[LPT], const uint4 (&vx)[LPT], int stg) {
+    char *Ks = ring + stg * STAGE, *Vs = Ks + KB;
 #pragma unroll
-    for (int u = 0; u < KLD; ++u) {
+    for (int u = 0; u < LPT; ++u) {
       const int x = tid + u * NTH;
-      const int kk = x / CPR, c = x % CPR;
-      *reinterpret_cast<uint4 *>(Ks + kk * KSTR + c * 16) = kreg[u];
-    }
-#pragma unroll
-    for (int u = 0; u < VLD; ++u) {
-      const int x = tid + u * NTH;
-      if (VTASK % NTH == 0 || x < VTASK) {
-        const int kg = x % (KT / TK), c = x / (KT / TK);
-        const int kk0 = kg * TK;
-        const int pos0 = (kk0 & ~31) | (((kk0 >> 2) & 3) << 3) | (((kk0 >> 4) & 1) << 2) |
-                         (kk0 & 3);
-        const uint32_t w0[4] = {vreg[u][0].x, vreg[u][0].y, vreg[u][0].z, vreg[u][0].w};
-        const uint32_t w1[4] = {vreg[u][1].x, vreg[u][1].y, vreg[u][1].z, vreg[u][1].w};
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          // d = 8c + 2p (low halves) and 8c + 2p + 1 (high halves)
-          const uint32_t lo01 = __builtin_amdgcn_perm(w1[p], w0[p], 0x05040100u);
-          const uint32_t hi01 = __builtin_amdgcn_perm(w1[p], w0[p], 0x07060302u);
-          char *dlo = Vt + (8 * c + 2 * p) * VSTR + pos0 * 2;
-          char *dhi = Vt + (8 * c + 2 * p + 1) * VSTR + pos0 * 2;
-          if (TK == 4) {
-            const uint32_t w2 = (&vreg[u][TK > 2 ? 2 : 0].x)[p];
-            const uint32_t w3 = (&vreg[u][TK > 2 ? 3 : 0].x)[p];
-            *reinterpret_cast<uint2 *>(dlo) =
-                make_uint2(lo01, __builtin_amdgcn_perm(w3, w2, 0x05040100u));
-            *reinterpret_cast<uint2 *>(dhi) =
-                make_uint2(hi01, __builtin_amdgcn_perm(w3, w2, 0x07060302u));
-          } else {
-            *reinterpret_cast<uint32_t *>(dlo) = lo01;
-            *reinterpret_cast<uint32_t *>(dhi) = hi01;
-          }
-        }
-      }
+      const int row = x / CPR, c = x % CPR;
+      const int fk = (row >> RSH) & (CPR - 1);
+      const int fv = 2 * ((row >> RSH) & (CPR / 2 - 1));
+      *reinterpret_cast<uint4 *>(Ks + row * ROWB + 16 * (c ^ fk)) = kx[u];
+      *reinterpret_cast<uint4 *>(Vs + row * ROWB + 16 * (c ^ fv)) = vx[u];
     }
   };
 
-  // pipeline `pipe` takes tiles pipe, pipe + P, ... of [k_begin, k_end)
-  const int64_t ntile = (k_end - k_begin + KT - 1) / KT;
-  const int64_t iters = (ntile + P - 1) / P;
-  auto tile_start = [&](int64_t it) { return k_begin + (P * it + pipe) * KT; };
-  if (iters > 0 && tile_start(0) < k_end) {
-    fetch(tile_start(0));
-    stash(0);
+  // o[cb][NDB] accumulates the softmax denominator (a block of ones times P^T)
+  f32x4 o[CB][NDB + 1];
+  float m_run[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    m_run[cb] = -INFINITY;  // reference max of raw scores
+#pragma unroll
+    for (int db = 0; db <= NDB; ++db) o[cb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // The Q fragments stay in registers for the whole key loop: wait for them
-  // here (their loads overlapped the first tile's) so that no wait on them
-  // is left for the loop body.
+  const bf16x8 ones = as_bf16x8(make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u));
+  // LDS read offsets inside a stage. K: row 16 kb + l16, chunk 4 ks + q4.
+  // Transposed V: this lane supplies the address of row 16 hv + 4 q4 + l16 / 4,
+  // d = 16 db + 4 (l16 % 4), i.e. chunk 2 db + (l16 % 4) / 2, byte 8 (l16 % 2).
+  int kofs[2][NKS];
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) asm volatile("" ::"v"(qf[ks]));
-  __syncthreads();
-  int cur = 0;
-  for (int64_t it = 0; it < iters; ++it) {
-    const int64_t t0 = tile_start(it);
-    const bool active = t0 < k_end;                 // uniform per pipeline
-    const bool more = tile_start(it + 1) < k_end;
-    if (more) fetch(tile_start(it + 1));            // in flight during this tile
-    if (active) {
-      const char *Ks = my + cur * STAGE, *Vt = Ks + KBYTES;
-      // S^T (keys x queries), one 16-key block at a time; lane (l16, q4)
-      // holds keys 16kb + 4q4 + j of query column l16
-      f32x4 s[NKB];
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        bf16x8 a[NKS];
+    for (int ks = 0; ks < NKS; ++ks) {
+      const int row = 16 * kb + l16;
+      kofs[kb][ks] = row * ROWB + 16 * ((4 * ks + q4) ^ ((row >> RSH) & (CPR - 1)));
+    }
+  int vofs[2], vf[2];
+#pragma unroll
+  for (int hv = 0; hv < 2; ++hv) {
+    const int row = 16 * hv + 4 * q4 + (l16 >> 2);
+    vofs[hv] = KB + row * ROWB + 8 * (l16 & 1);
+    vf[hv] = 2 * ((row >> RSH) & (CPR / 2 - 1));
+  }
+  const int vchk = (l16 & 3) >> 1;
+
+  auto compute = [&](int it) {
+    const int nvalid = tile(it).nvalid;
+    const char *stg = ring + (it & 1) * STAGE;
+    // S^T (keys x queries), one 16-key block at a time; lane (l16, q4)
+    // holds keys 16 kb + 4 q4 + j of query column l16 of each column block
+    f32x4 s[2][CB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 a[NKS];
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+        a[ks] = as_bf16x8(*reinterpret_cast<const uint4 *>(stg + kofs[kb][ks]));
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        s[kb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
-          a[ks] = as_bf16x8(*reinterpret_cast<const uint4 *>(
-              Ks + (16 * kb + l16) * KSTR + (32 * ks + 8 * q4) * 2));
-        s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-          s[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], qf[ks], s[kb], 0, 0, 0);
-      }
-      // online softmax on raw scores; the scale and log2(e) enter through
-      // one FMA in the exp2 argument
-      if (t0 + KT > k_end) {  // last, partial tile
-        asm volatile("");     // keep this a branch: full tiles skip it
-        const int lim = (int)(k_end - t0);
-#pragma unroll
-        for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (16 * kb + 4 * q4 + j >= lim) s[kb][j] = -INFINITY;
-      }
-      float mx = s[0][0];
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) mx = fmaxf(mx, s[kb][j]);
-      mx = max4q(mx);
-      // Lazy rescaling: the reference max m_run moves only when a row's max
-      // exceeds it by more than 2^8 in probability (or on the first tile);
-      // otherwise probabilities up to 256 are accumulated against the old
-      // reference, which bf16 P and fp32 O hold exactly as well.
-      if (__ballot((mx - m_run) * sl2 > 8.f)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
-#pragma unroll
-        for (int db = 0; db < NDB + 1; ++db) o[db] *= alpha;
-        m_run = m_new;
-      }
-      const float nb = -m_run * sl2;
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s[kb][j] = __builtin_amdgcn_exp2f(fmaf(s[kb][j], sl2, nb));
-      // O^T += V^T P^T, one 32-key k-step at a time; the extra block of
-      // ones gives the softmax denominator from the same bf16 P
-#pragma unroll
-      for (int ps = 0; ps < NPS; ++ps) {
-        uint4 pw;
-        pw.x = pack2(s[2 * ps][0], s[2 * ps][1]);
-        pw.y = pack2(s[2 * ps][2], s[2 * ps][3]);
-        pw.z = pack2(s[2 * ps + 1][0], s[2 * ps + 1][1]);
-        pw.w = pack2(s[2 * ps + 1][2], s[2 * ps + 1][3]);
-        const bf16x8 pb = as_bf16x8(pw);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4 *>(
-              Vt + (16 * db + l16) * VSTR + (32 * ps + 8 * q4) * 2));
-          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, o[db], 0, 0, 0);
-        }
-        o[NDB] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb, o[NDB], 0, 0, 0);
+          s[kb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], qf[cb][ks], s[kb][cb], 0, 0, 0);
       }
     }
-    if (more) stash(cur ^ 1);
-    __syncthreads();
-    cur ^= 1;
+    if (nvalid < KT) {      // partial (or, past the split's end, empty) tile
+      asm volatile("");     // keep this a branch: full tiles skip it
+      const int lim = nvalid;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (16 * kb + 4 * q4 + j >= lim) s[kb][cb][j] = -INFINITY;
+    }
+    // online softmax on raw scores; the scale and log2(e) enter through one
+    // FMA in the exp2 argument. Lazy rescaling: the reference max moves only
+    // when a row's max exceeds it by more than 2^8 in probability (or on the
+    // first tile); probabilities up to 256 are accumulated against the old
+    // reference, which bf16 P and fp32 O hold exactly as well.
+    bf16x8 pb[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      float mx = s[0][cb][0];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mx = fmaxf(mx, s[kb][cb][j]);
+      mx = max4q(mx);
+      if (__ballot((mx - m_run[cb]) * sl2 > 8.f)) {
+        const float m_new = fmaxf(m_run[cb], mx);
+        const float alpha = __builtin_amdgcn_exp2f((m_run[cb] - m_new) * sl2);
+#pragma unroll
+        for (int db = 0; db <= NDB; ++db) o[cb][db] *= alpha;
+        m_run[cb] = m_new;
+      }
+      // (a pipeline whose tiles were all empty so far has no reference yet;
+      // its fully masked scores then give exp2(-inf) = 0)
+      const float nb = m_run[cb] == -INFINITY ? 0.f : -m_run[cb] * sl2;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          s[kb][cb][j] = __builtin_amdgcn_exp2f(fmaf(s[kb][cb][j], sl2, nb));
+      // B operand slots 0..3: keys 4 q4 + j; slots 4..7: keys 16 + 4 q4 + j
+      uint4 pw;
+      pw.x = pack2(s[0][cb][0], s[0][cb][1]);
+      pw.y = pack2(s[0][cb][2], s[0][cb][3]);
+      pw.z = pack2(s[1][cb][0], s[1][cb][1]);
+      pw.w = pack2(s[1][cb][2], s[1][cb][3]);
+      pb[cb] = as_bf16x8(pw);
+    }
+    // O^T += V^T P^T: the A operand of d-block db is read transposed from the
+    // row-major V tile, in the key order of the B slots above
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const int c = 2 * db + vchk;
+      const uint2 lo = lds_tr16(stg + vofs[0] + 16 * (c ^ vf[0]));
+      const uint2 hi = lds_tr16(stg + vofs[1] + 16 * (c ^ vf[1]));
+      const bf16x8 av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        o[cb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb[cb], o[cb][db], 0, 0, 0);
+    }
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+      o[cb][NDB] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[cb], o[cb][NDB], 0, 0, 0);
+  };
+
+  // Prologue: tiles 0 and 1 into the two register sets, tile 0 into LDS
+  // stage 0, tile 2 into the set it freed. Fetches and stashes run for every
+  // round, also past this pipeline's last tile (those re-read the split's
+  // last row, in bounds, and are never consumed): the number of loads in
+  // flight is then the same on every path, which lets the compiler wait for
+  // exactly the set being stashed and keep the other one in flight.
+  fetch(kr[0], vr[0], 0);
+  fetch(kr[1], vr[1], 1);
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) asm volatile("" ::"v"(qf[cb][ks]));
+  stash(kr[0], vr[0], 0);
+  fetch(kr[0], vr[0], 2);
+  lds_barrier();
+  // Round it: tile it + 1 (register set (it + 1) & 1) goes to LDS stage
+  // (it + 1) & 1, tile it + 3 is fetched into that set, tile it is consumed
+  // from stage it & 1. The loop is unrolled by two so that the register sets
+  // are named statically.
+  // The two waves that share a SIMD belong to pipelines p and p + 2; the
+  // first half of the pipelines computes before it stashes and fetches, the
+  // second half after, so that one wave's MFMA work meets the other's memory
+  // and VALU work instead of the same unit.
+  const bool compute_first = pipe < P / 2;
+  auto round = [&](int it, uint4 (&kn)[LPT], uint4 (&vn)[LPT]) {
+    if (compute_first) compute(it);
+    stash(kn, vn, (it + 1) & 1);
+    fetch(kn, vn, it + 3);
+    if (!compute_first) compute(it);
+    lds_barrier();
+  };
+  // (an odd round count gets one idle round: both halves of the unrolled body
+  // always run, so the loads in flight at the loop head are the same on
+  // every path into it)
+  for (int it = 0; it < rounds; it += 2) {
+    round(it, kr[1], vr[1]);
+    round(it + 1, kr[0], vr[0]);
   }
 
   // merge pipelines 1..P-1 into pipeline 0 through LDS (same rows and lanes)
-  if (P > 1) {
-    constexpr int SLOT = (NDB + 1) * 4 + 1;
+  if constexpr (P > 1) {
+    constexpr int SLOT = CB * ((NDB + 1) * 4 + 1) + 1;  // odd: no bank conflicts
     float *xs = reinterpret_cast<float *>(smem);
     if (pipe > 0) {
-      float *x = xs + ((size_t)(pipe - 1) * NTH + tid) * SLOT;
+      float *x = xs + ((size_t)((pipe - 1) * NWP + w) * 64 + lane) * SLOT;
 #pragma unroll
-      for (int db = 0; db <= NDB; ++db)
+      for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) x[db * 4 + j] = o[db][j];
-      x[(NDB + 1) * 4] = m_run;
+        for (int db = 0; db <= NDB; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) x[cb * ((NDB + 1) * 4 + 1) + db * 4 + j] = o[cb][db][j];
+        x[cb * ((NDB + 1) * 4 + 1) + (NDB + 1) * 4] = m_run[cb];
+      }
     }
-    __syncthreads();
-    if (pipe > 0 || !rvalid) return;
+    lds_barrier();
+    if (pipe > 0) return;
 #pragma unroll 1
     for (int pp = 1; pp < P; ++pp) {
-      const float *x = xs + ((size_t)(pp - 1) * NTH + tid) * SLOT;
-      const float m1 = x[(NDB + 1) * 4];
-      const float mm = fmaxf(m_run, m1);
-      const float a0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - mm) * sl2);
-      const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mm) * sl2);
+      const float *x = xs + ((size_t)((pp - 1) * NWP + w) * 64 + lane) * SLOT;
 #pragma unroll
-      for (int db = 0; db <= NDB; ++db)
+      for (int cb = 0; cb < CB; ++cb) {
+        const float *xc = x + cb * ((NDB + 1) * 4 + 1);
+        const float m1 = xc[(NDB + 1) * 4];
+        const float mm = fmaxf(m_run[cb], m1);
+        const float a0 =
+            m_run[cb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run[cb] - mm) * sl2);
+        const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mm) * sl2);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) o[db][j] = o[db][j] * a0 + x[db * 4 + j] * a1;
-      m_run = mm;
+        for (int db = 0; db <= NDB; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[cb][db][j] = o[cb][db][j] * a0 + xc[db * 4 + j] * a1;
+        m_run[cb] = mm;
+      }
     }
-  } else if (!rvalid) {
-    return;
   }
-  const float l_run = o[NDB][0];
-  // lane holds d = 16db + 4q4 + j of query row r
-  if (nsplit == 1) {
-    const float inv = 1.f / l_run;
-    uint16_t *orow = out + qoff;
+  // lane holds d = 16 db + 4 q4 + j of query row rbase + 16 cb + l16
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      uint2 w;
-      w.x = pack2(o[db][0] * inv, o[db][1] * inv);
-      w.y = pack2(o[db][2] * inv, o[db][3] * inv);
-      *reinterpret_cast<uint2 *>(orow + 16 * db + 4 * q4) = w;
+  for (int cb = 0; cb < CB; ++cb) {
+    if (!rvalid[cb]) continue;
+    const int r = rbase + 16 * cb + l16;
+    const float l_run = o[cb][NDB][0];
+    if (nsplit == 1) {
+      const float inv = 1.f / l_run;
+      uint16_t *orow = out + qoff[cb];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        uint2 wd;
+        wd.x = pack2(o[cb][db][0] * inv, o[cb][db][1] * inv);
+        wd.y = pack2(o[cb][db][2] * inv, o[cb][db][3] * inv);
+        *reinterpret_cast<uint2 *>(orow + 16 * db + 4 * q4) = wd;
+      }
+    } else {
+      const int64_t pidx = ((int64_t)b * Hkv + h) * nsplit + split;
+      float *po = part_o + (pidx * M + r) * D;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        *reinterpret_cast<float4 *>(po + 16 * db + 4 * q4) =
+            make_float4(o[cb][db][0], o[cb][db][1], o[cb][db][2], o[cb][db][3]);
+      if (q4 == 0) part_ml[pidx * M + r] = make_float2(m_run[cb] * sl2, l_run);
     }
-  } else {
-    const int64_t pidx = ((int64_t)b * Hkv + h) * nsplit + split;
-    float *po = part_o + (pidx * M + r) * D;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      *reinterpret_cast<float4 *>(po + 16 * db + 4 * q4) =
-          make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
-    if (q4 == 0) part_ml[pidx * M + r] = make_float2(m_run * sl2, l_run);
   }
 }
 
@@ -487,15 +563,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   }
 }
 
-// Query rows per workgroup (128 or 64); read once per process.
-int max_rows_per_wg() {
-  static const int r = [] {
-    const char *v = getenv("HERALD_ATTN_ROWS");
-    return (v && atoi(v) == 128) ? 128 : 64;
-  }();
-  return r;
-}
-
 // Workgroups the split-KV plan aims for; read once per process.
 int target_wgs() {
   static const int t = [] {
@@ -520,13 +587,17 @@ AttnPlan attn_plan(const herald_heads &hd, int batch, int block, int64_t max_ctx
     p.n_mblk = (p.M + 3) / 4;
     return p;
   }
-  // waves of 16 rows; 128-row blocks run 2 pipelines of 64-key tiles, smaller
-  // blocks 4 pipelines of 32-key tiles (both fill one CU's LDS)
-  const int rows = max_rows_per_wg();
-  p.nwaves = (p.M > 64 && rows >= 128) ? 8 : (p.M > 32 ? 4 : (p.M > 16 ? 2 : 1));
-  p.pipes = p.nwaves == 8 ? 2 : 4;
-  p.key_tile = p.nwaves == 8 ? 64 : 32;
-  p.n_mblk = (p.M + 16 * p.nwaves - 1) / (16 * p.nwaves);
+  // Row blocks of 64 rows: 4 pipelines of 2 waves x 32 rows (512 threads);
+  // blocks of at most 32 rows: 4 pipelines of one wave.
+  p.pipes = 4;
+  p.stages = 2;
+  p.key_tile = 32;
+  if (p.M > 32) {
+    p.rows_per_wave = 32, p.nwaves = 2;
+  } else {
+    p.rows_per_wave = p.M > 16 ? 32 : 16, p.nwaves = 1;
+  }
+  p.n_mblk = (p.M + p.rows_per_wave * p.nwaves - 1) / (p.rows_per_wave * p.nwaves);
   const int64_t max_keys = max_ctx + block;
   const int64_t ntile = (max_keys + p.key_tile - 1) / p.key_tile;
   const int64_t base = (int64_t)batch * hd.num_kv_heads * p.n_mblk;
@@ -579,26 +650,22 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, const
   const uint16_t *bk = (const uint16_t *)blk_k, *bv = (const uint16_t *)blk_v;
   uint16_t *oo = (uint16_t *)out;
   const bool paged = ctx.pt != nullptr;
-#define HERALD_ATTN(D_, NW_, P_, KT_, PG_)                                               \
-  if (D == D_ && p.nwaves == NW_ && paged == PG_) {                                      \
-    auto kfn = attn_bf16_kernel<D_, NW_, P_, KT_, PG_>;                                  \
-    constexpr int kSmem = 2 * P_ * (KT_ * (D_ * 2 + 16) + D_ * (KT_ * 2 + 16));          \
+#define HERALD_ATTN(D_, RW_, NW_, PG_)                                                   \
+  if (D == D_ && p.rows_per_wave == RW_ && p.nwaves == NW_ && paged == PG_) {            \
+    auto kfn = attn_bf16_kernel<D_, RW_, NW_, 4, PG_>;                                    \
+    constexpr int kSmem = attn_smem_bytes<D_, RW_, NW_, 4>();                             \
     static const hipError_t attr_err = hipFuncSetAttribute(                               \
         reinterpret_cast<const void *>(kfn), hipFuncAttributeMaxDynamicSharedMemorySize,  \
         kSmem);                                                                          \
     if (attr_err != hipSuccess) return attr_err;                                         \
-    kfn<<<grid, NW_ * P_ * 64, kSmem, stream>>>(qq, ctx, bk, bv, oo, part_o, part_ml,     \
-                                                block, Hq, Hkv, G, p.M, p.n_mblk,        \
-                                                p.nsplit, p.keys_per_split, sl2);        \
+    kfn<<<grid, NW_ * 4 * 64, kSmem, stream>>>(qq, ctx, bk, bv, oo, part_o, part_ml,      \
+                                               block, Hq, Hkv, G, p.M, p.n_mblk,         \
+                                               p.nsplit, p.keys_per_split, sl2);         \
   } else
-  HERALD_ATTN(64, 8, 2, 64, false) HERALD_ATTN(64, 4, 4, 32, false)
-  HERALD_ATTN(64, 2, 4, 32, false) HERALD_ATTN(64, 1, 4, 32, false)
-  HERALD_ATTN(128, 8, 2, 64, false) HERALD_ATTN(128, 4, 4, 32, false)
-  HERALD_ATTN(128, 2, 4, 32, false) HERALD_ATTN(128, 1, 4, 32, false)
-  HERALD_ATTN(64, 8, 2, 64, true) HERALD_ATTN(64, 4, 4, 32, true)
-  HERALD_ATTN(64, 2, 4, 32, true) HERALD_ATTN(64, 1, 4, 32, true)
-  HERALD_ATTN(128, 8, 2, 64, true) HERALD_ATTN(128, 4, 4, 32, true)
-  HERALD_ATTN(128, 2, 4, 32, true) HERALD_ATTN(128, 1, 4, 32, true)
+  HERALD_ATTN(64, 32, 2, false) HERALD_ATTN(64, 32, 1, false) HERALD_ATTN(64, 16, 1, false)
+  HERALD_ATTN(128, 32, 2, false) HERALD_ATTN(128, 32, 1, false) HERALD_ATTN(128, 16, 1, false)
+  HERALD_ATTN(64, 32, 2, true) HERALD_ATTN(64, 32, 1, true) HERALD_ATTN(64, 16, 1, true)
+  HERALD_ATTN(128, 32, 2, true) HERALD_ATTN(128, 32, 1, true) HERALD_ATTN(128, 16, 1, true)
   return hipErrorInvalidValue;
 #undef HERALD_ATTN
   if (p.nsplit > 1) {

@@ -112,8 +112,10 @@ hipError_t launch_gather(const herald_heads &hd, int batch, const KvView &kv,
 
 struct AttnPlan {
   int M;          // G * block query rows per (b, h)
-  int nwaves;     // waves per pipeline (16 query rows each)
+  int rows_per_wave; // query rows per wave (16 or 32)
+  int nwaves;     // waves per pipeline
   int pipes;      // pipelines per workgroup (alternate key tiles)
+  int stages;     // LDS stages per pipeline
   int key_tile;   // keys per tile
   int n_mblk;     // row blocks per (b, h)
   int nsplit;     // key splits of this call
