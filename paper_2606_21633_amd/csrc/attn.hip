@@ -122,22 +122,25 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
   // Workgroups are dealt round-robin to the 8 XCDs by linear id. When the row
   // blocks of one KV head split its query rows, place them on the same XCD
   // (ids id and id + 8, ...) so that their shared K/V tiles hit its L2.
-  int split = blockIdx.x, b = blockIdx.z, h, mblk;
+  // The grid is 1-D over (group, row block), a group being one (sequence, KV
+  // head, key split). Workgroups are dealt round-robin to the 8 XCDs by id;
+  // the row blocks of one group get ids id, id + 8, ... so that they run on
+  // one XCD at the same time and share its L2 for their common K/V tiles.
+  const int n_groups = gridDim.x / n_mblk;
+  int grp, mblk;
   {
-    const int y = blockIdx.y;
-    h = y / n_mblk;
-    mblk = y % n_mblk;
-    const int pairs = gridDim.y / n_mblk * gridDim.z;   // (b, h) pairs
-    if (gridDim.x == 1 && n_mblk > 1 && pairs % 8 == 0) {
-      const int id = y + gridDim.y * blockIdx.z;
-      const int slot = id / 8;
+    const int id = blockIdx.x;
+    if (n_mblk > 1 && n_groups % 8 == 0) {
+      const int slot = id >> 3;
       mblk = slot % n_mblk;
-      const int pair = (slot / n_mblk) * 8 + id % 8;
-      const int hk = gridDim.y / n_mblk;
-      b = pair / hk;
-      h = pair % hk;
+      grp = (slot / n_mblk) * 8 + (id & 7);
+    } else {
+      mblk = id % n_mblk;
+      grp = id / n_mblk;
     }
   }
+  const int split = grp % nsplit;
+  const int h = (grp / nsplit) % Hkv, b = grp / nsplit / Hkv;
   const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int pipe = wv / NWP, w = wv % NWP;
   const int tid = threadIdx.x % NTH, lane = threadIdx.x & 63, q4 = lane >> 4, l16 = lane & 15;
@@ -645,7 +648,7 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, const
   float *part_o = reinterpret_cast<float *>(w);
   float2 *part_ml = reinterpret_cast<float2 *>(w + ((p.part_o_bytes + 255) & ~(size_t)255));
   const float sl2 = (float)(1.0 / sqrt((double)D)) * kLog2e;
-  const dim3 grid(p.nsplit, Hkv * p.n_mblk, batch);
+  const int grid = batch * Hkv * p.nsplit * p.n_mblk;
   const uint16_t *qq = (const uint16_t *)q;
   const uint16_t *bk = (const uint16_t *)blk_k, *bv = (const uint16_t *)blk_v;
   uint16_t *oo = (uint16_t *)out;
