@@ -191,6 +191,31 @@ def main():
                          stream=s_main)
     with torch.cuda.stream(s_main):
         ms_attn = timed(denoise_phase, 1, s_main) / n_att
+        # per-launch spread: an event between consecutive launches
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(min(n_att, 256) + 1)]
+        evs[0].record(s_main)
+        for j in range(len(evs) - 1):
+            t = j % T
+            H.block_attn(hd, b, B, q_steps[t], ctx_kv, blk_k[t], blk_v[t], out, ws_att,
+                         stream=s_main)
+            evs[j + 1].record(s_main)
+        torch.cuda.synchronize()
+        per = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(len(evs) - 1)])
+        # cold: one launch right after writing 512 MiB, so that neither L2 nor
+        # the last-level cache holds the pool
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        cold = []
+        for j in range(10):
+            flush.fill_(j)
+            c0 = torch.cuda.Event(enable_timing=True)
+            c1 = torch.cuda.Event(enable_timing=True)
+            c0.record(s_main)
+            H.block_attn(hd, b, B, q_steps[j % T], ctx_kv, blk_k[j % T], blk_v[j % T], out,
+                         ws_att, stream=s_main)
+            c1.record(s_main)
+            torch.cuda.synchronize()
+            cold.append(c0.elapsed_time(c1))
+        del flush
         ms_sel = timed(lambda: H.select(hd, b, B, q_next, kv_cache, kps, k_max, idx, ws_sel,
                                         stream=s_main), max(5, args.reps // 3), s_main)
         ms_gat = timed(lambda: H.gather(hd, b, kv_cache, idx, kps, k_max,
@@ -238,7 +263,12 @@ def main():
                      "ms": round(ms_attn, 5), "launches_timed": n_att,
                      "bytes_per_launch": attn_bytes,
                      "flops_per_launch": attn_flops, "TFLOPs": round(attn_tflops, 2),
-                     "mfma_frac": round(attn_tflops / peak, 4)},
+                     "mfma_frac": round(attn_tflops / peak, 4),
+                     "ms_p10_p50_p90": [round(float(np.percentile(per, x)), 5)
+                                        for x in (10, 50, 90)],
+                     "cold_ms_p50": round(float(np.median(cold)), 5),
+                     "cold_frac": round(attn_bytes / (np.median(cold) * 1e-3) / 1e9
+                                        / HBM_PEAK_GBPS, 4)},
         "selection": {"ms": round(ms_sel, 5), "k_bytes": sel_bytes,
                       "scan_GBps": round(sel_gbps, 1),
                       "frac_hbm": round(sel_gbps / HBM_PEAK_GBPS, 4)},

@@ -1,9 +1,10 @@
 """Text summaries of rocprofv3 CSV output for the kernels of libherald.so.
 
-    python -m paper_2606_21633_amd.profsum trace DIR [--kernel NAME --last N]
+    python -m paper_2606_21633_amd.profsum trace DIR [--kernel NAME --last N --skip-last M]
         per-kernel launch statistics from DIR/*kernel_trace.csv; with --kernel,
-        also the average duration of that kernel's last N launches (the
-        denoising phase that bench.py times with HIP events).
+        also the average duration of N of that kernel's launches, the last N
+        before its final M (the denoising phase that bench.py times with HIP
+        events, followed by M launches timed one by one).
 
     python -m paper_2606_21633_amd.profsum traffic --fetch DIR --write DIR
             --copy-fetch DIR --copy-write DIR --copy-bytes B --kernel NAME
@@ -60,12 +61,15 @@ def trace(args) -> None:
         v = [x for n, x in ((_short(r["Kernel_Name"]),
                              (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
                             for r in rows) if n.startswith(args.kernel)]
+        if args.skip_last:
+            v = v[:-args.skip_last]
         tail = v[-args.last:] if args.last else v
-        print(f"\n{args.kernel}: last {len(tail)} launches: avg {sum(tail) / len(tail):.2f} us, "
+        print(f"\n{args.kernel}: {len(tail)} launches (the last {args.last} before the final "
+              f"{args.skip_last}): avg {sum(tail) / len(tail):.2f} us, "
               f"min {min(tail):.2f} us, max {max(tail):.2f} us")
 
 
-def _counter(d: str, counter: str, kernel: str, last: int):
+def _counter(d: str, counter: str, kernel: str, last: int, skip_last: int = 0):
     rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))))
     per = {}
     for r in rows:
@@ -77,6 +81,8 @@ def _counter(d: str, counter: str, kernel: str, last: int):
         per.setdefault(int(r["Dispatch_Id"]), 0.0)
         per[int(r["Dispatch_Id"])] += float(r["Counter_Value"])
     vals = [per[k] for k in sorted(per)]
+    if skip_last:
+        vals = vals[:-skip_last]
     if not vals:
         sys.exit(f"no {counter} values for {kernel} in {d}")
     vals = vals[-last:] if last else vals
@@ -84,8 +90,8 @@ def _counter(d: str, counter: str, kernel: str, last: int):
 
 
 def traffic(args) -> None:
-    f_kib, nf = _counter(args.fetch, "FETCH_SIZE", args.kernel, args.last)
-    w_kib, nw = _counter(args.write, "WRITE_SIZE", args.kernel, args.last)
+    f_kib, nf = _counter(args.fetch, "FETCH_SIZE", args.kernel, args.last, args.skip_last)
+    w_kib, nw = _counter(args.write, "WRITE_SIZE", args.kernel, args.last, args.skip_last)
     cf_kib, _ = _counter(args.copy_fetch, "FETCH_SIZE", args.copy_kernel, 0)
     cw_kib, _ = _counter(args.copy_write, "WRITE_SIZE", args.copy_kernel, 0)
     sf = args.copy_bytes / (cf_kib * 1024.0)
@@ -110,6 +116,7 @@ def main(argv=None) -> None:
     t.add_argument("dir")
     t.add_argument("--kernel", default="")
     t.add_argument("--last", type=int, default=0)
+    t.add_argument("--skip-last", type=int, default=0)
     c = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy_fetch", "copy_write"):
         c.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
@@ -117,6 +124,7 @@ def main(argv=None) -> None:
     c.add_argument("--copy-kernel", default="vectorized_elementwise_kernel")
     c.add_argument("--kernel", required=True)
     c.add_argument("--last", type=int, default=0)
+    c.add_argument("--skip-last", type=int, default=0)
     c.add_argument("--source-sha256", default="")
     args = ap.parse_args(argv)
     (trace if args.cmd == "trace" else traffic)(args)
