@@ -201,12 +201,13 @@ def main():
             evs[j + 1].record(s_main)
         torch.cuda.synchronize()
         per = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(len(evs) - 1)])
-        # cold: one launch right after writing 512 MiB, so that neither L2 nor
-        # the last-level cache holds the pool
-        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        # cold: one launch right after reading 512 MiB of other data, so that
+        # neither L2 nor the last-level cache holds the pool (a read leaves no
+        # dirty lines whose write-back the timed launch would pay for)
+        flush = torch.ones(512 << 20, dtype=torch.uint8, device=dev)
         cold = []
         for j in range(10):
-            flush.fill_(j)
+            flush.max()
             c0 = torch.cuda.Event(enable_timing=True)
             c1 = torch.cuda.Event(enable_timing=True)
             c0.record(s_main)
