@@ -56,22 +56,22 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
     const int64_t step = (int64_t)Hq * D;
     double acc = 0.0;
     for (int i0 = 0; i0 < block; i0 += U) {
+      // every load is issued (rows past the block re-read its last row) so
+      // that all of them are in flight together; the sum takes only the
+      // block's rows, in block-row order
       float x[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int i = i0 + u;
-        x[u] = 0.f;
-        if (i < block) {
-          if (BF16)
-            x[u] = __uint_as_float(
-                (uint32_t)reinterpret_cast<const uint16_t *>(q_sel)[base + i * step] << 16);
-          else
-            x[u] = reinterpret_cast<const float *>(q_sel)[base + i * step];
-        }
+        const int i = min(i0 + u, block - 1);
+        if (BF16)
+          x[u] = __uint_as_float(
+              (uint32_t)reinterpret_cast<const uint16_t *>(q_sel)[base + i * step] << 16);
+        else
+          x[u] = reinterpret_cast<const float *>(q_sel)[base + i * step];
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (i0 + u < block) acc += (double)x[u];  // block-row order
+      for (int u = 0; u < U; ++u)  // (past the block: + 0.0, which leaves acc as is)
+        acc += i0 + u < block ? (double)x[u] : 0.0;
     }
     qbar[(bh * D + e) * G + g] = acc / (double)block;
   }
