@@ -177,3 +177,87 @@ def test_pipeline_layer32k_shapes_one_block():
                      S_hi=8192, seed=4)
     outs, _ = run_gpu(case)
     check_against_oracle(case, outs)
+
+
+def test_pipeline_36_layer_workload_shape_sampled():
+    """The 36-layer workload's per-layer shape (8 sequences x 65536 tokens,
+    32 query / 8 KV heads, B=32, 5% budget) with its device-side generator,
+    two layers and T=2 steps per block, two pipelined blocks; sequences 0 and
+    5 of both layers are checked against the oracle's sequential schedule."""
+    import dataclasses
+    wl = dataclasses.replace(synth.PIPELINE_36L, layers=2, steps=2)
+    b, B, T, L = wl.batch, wl.block, wl.steps, wl.layers
+    Hq, Hkv, d, S0 = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.seq_len
+    nblocks = 2
+    cap = S0 + (nblocks + 1) * B
+    data = synth.make_device_layers(wl, DEV, capacity=cap)
+    gen = data["gen"]
+    hd = H.heads(Hq, Hkv, d, "bf16")
+    k_hi = H.budget_tokens(cap, *wl.budget)
+    pcap = k_hi + B
+    lay = []
+    for l in range(L):
+        u = data["u"][l]
+        lay.append(dict(
+            k=data["k"][l], v=data["v"][l], q_sel0=synth.device_queries(wl, u, gen, (), DEV),
+            pools=[[torch.zeros((b, Hkv, pcap, d), dtype=torch.bfloat16, device=DEV)
+                    for _ in range(2)] for _ in range(2)],
+            out=torch.zeros((T, b, B, Hq, d), dtype=torch.bfloat16, device=DEV),
+            blocks=[dict(q=synth.device_queries(wl, u, gen, (T,), DEV),
+                         bk=synth.device_normal(wl, gen, (T, b, B, Hkv, d), DEV),
+                         bv=synth.device_normal(wl, gen, (T, b, B, Hkv, d), DEV),
+                         dk=synth.device_normal(wl, gen, (b, B, Hkv, d), DEV),
+                         dvv=synth.device_normal(wl, gen, (b, B, Hkv, d), DEV),
+                         qn=synth.device_queries(wl, u, gen, (), DEV))
+                    for _ in range(nblocks)]))
+    samp = (0, 5)
+    # host copies for the oracle, taken before the pipeline appends blocks
+    host = {(l, i): (to_host(lay[l]["k"][i, :, :S0]), to_host(lay[l]["v"][i, :, :S0]))
+            for l in range(L) for i in samp}
+    lens = torch.full((b,), S0, dtype=torch.int32, device=DEV)
+    k0 = H.budget_tokens(S0, *wl.budget)
+    kps0 = torch.full((b,), k0, dtype=torch.int32, device=DEV)
+    idx = torch.empty((b, Hkv, k0), dtype=torch.int32, device=DEV)
+    wsel = H.workspace(H.select_workspace(hd, b, S0), DEV)
+    for Ly in lay:
+        kv = H.kv_view(Ly["k"], Ly["v"], lens, S0)
+        H.select(hd, b, B, Ly["q_sel0"], kv, kps0, k0, idx, wsel)
+        H.gather(hd, b, kv, idx, kps0, k0, H.pool_view(*Ly["pools"][0]))
+    n_pool = [kps0.clone(), torch.zeros(b, dtype=torch.int32, device=DEV)]
+    s_main, s_retr = torch.cuda.Stream(device=DEV), torch.cuda.Stream(device=DEV)
+    ws = H.workspace(H.decode_block_workspace(hd, b, B, cap, k_hi), DEV)
+    outs, a, S = [], 0, S0
+    for n in range(nblocks):
+        kn_h = H.budget_tokens(S, *wl.budget)
+        kn = torch.full((b,), kn_h, dtype=torch.int32, device=DEV)
+        layers = [H.Layer(H.pool_view(Ly["k"], Ly["v"]), H.pool_view(*Ly["pools"][a]),
+                          H.pool_view(*Ly["pools"][1 - a]), Ly["blocks"][n]["q"].data_ptr(),
+                          Ly["blocks"][n]["bk"].data_ptr(), Ly["blocks"][n]["bv"].data_ptr(),
+                          Ly["blocks"][n]["dk"].data_ptr(), Ly["blocks"][n]["dvv"].data_ptr(),
+                          Ly["blocks"][n]["qn"].data_ptr(), Ly["out"].data_ptr(),
+                          b * B * Hq * d) for Ly in lay]
+        torch.cuda.synchronize()
+        H.decode_block(hd, layers, b, B, T, lens, S, n_pool[a], pcap, n_pool[1 - a], kn, kn_h,
+                       False, ws, s_main, s_retr)
+        torch.cuda.synchronize()
+        outs.append([to_host(Ly["out"]).copy() for Ly in lay])
+        S += B
+        a = 1 - a
+    assert int(lens[0].item()) == S0 + nblocks * B
+    worst = 0.0
+    for l in range(L):
+        q0 = to_host(lay[l]["q_sel0"])
+        blocks_h = [{k: to_host(t) for k, t in blk.items()} for blk in lay[l]["blocks"]]
+        for i in samp:
+            K0, V0 = host[(l, i)]
+            idx0, _, _, _ = oracle.select(q0[i], K0, oracle.budget(S0, *wl.budget))
+            ref = oracle.decode_blocks(
+                K0, V0, idx0,
+                [dict(q_steps=bh["q"][:, i], k_steps=bh["bk"][:, i], v_steps=bh["bv"][:, i],
+                      k_done=bh["dk"][i], v_done=bh["dvv"][i], q_next=bh["qn"][i])
+                 for bh in blocks_h], *wl.budget)
+            for n in range(nblocks):
+                err = float(np.abs(f64(outs[n][l][:, i]) - ref[n]).max())
+                worst = max(worst, err)
+                assert err <= TOL, f"layer {l} seq {i} block {n}: {err}"
+    print(f"[pipeline 36L shape] max abs err {worst:.3g}")
