@@ -42,6 +42,8 @@ def parse():
                     choices=["layer32k", "long128k", "tiny", "ragged", "pipeline36"])
     ap.add_argument("--blocks", type=int, default=3,
                     help="timed blocks of the 36-layer pipeline workload")
+    ap.add_argument("--dense-layers", type=int, default=0,
+                    help="36-layer workload: how many first layers keep exact attention")
     ap.add_argument("--dense", action="store_true",
                     help="denoise over the full cache (GPU-only dense baseline)")
     ap.add_argument("--reps", type=int, default=30, help="isolated kernel timing reps")
@@ -445,6 +447,7 @@ def bench_pipeline36(args):
     Hq, Hkv, d, S0 = wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.seq_len
     nblk = args.warmup + args.blocks
     cap = S0 + (2 * nblk + 1) * B
+    nd = max(0, min(args.dense_layers, L))
     print(f"[bench] generating {wl.name} on the device", file=sys.stderr, flush=True)
     data = synth.make_device_layers(wl, dev, capacity=cap)
     gen = data["gen"]
@@ -479,7 +482,7 @@ def bench_pipeline36(args):
             kps0 = torch.full((b,), k0, dtype=torch.int32, device=dev)
             idx = torch.empty((b, Hkv, k0), dtype=torch.int32, device=dev)
             wsel = H.workspace(H.select_workspace(hd, b, S0), dev)
-            for Ly in layers:
+            for Ly in layers[nd:]:
                 kv = H.kv_view(Ly["k"], Ly["v"], lens, S0)
                 H.select(hd, b, B, Ly["qn"], kv, kps0, k0, idx, wsel)
                 H.gather(hd, b, kv, idx, kps0, k0, H.pool_view(*Ly["pools"][0]))
@@ -493,8 +496,8 @@ def bench_pipeline36(args):
             lay = [H.Layer(H.pool_view(Ly["k"], Ly["v"]), H.pool_view(*Ly["pools"][a]),
                            H.pool_view(*Ly["pools"][1 - a]), Ly["q"].data_ptr(),
                            Ly["bk"].data_ptr(), Ly["bv"].data_ptr(), Ly["dk"].data_ptr(),
-                           Ly["dvv"].data_ptr(), Ly["qn"].data_ptr(), Ly["out"].data_ptr(), 0)
-                   for Ly in layers]
+                           Ly["dvv"].data_ptr(), Ly["qn"].data_ptr(), Ly["out"].data_ptr(), 0,
+                           int(l < nd)) for l, Ly in enumerate(layers)]
             torch.cuda.synchronize()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
@@ -520,7 +523,8 @@ def bench_pipeline36(args):
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic, generated on the device (seeded torch generator)",
            "config": {"workload": wl.name, "layers": L, "batch": b, "seq_len": S0, "block": B,
-                      "steps": T, "budget": "5%", "step": "one block: next-block selection of "
+                      "steps": T, "budget": "5%", "dense_layers": nd,
+                      "step": "one block: next-block selection of "
                       "all layers on the retrieval stream, T x L denoising steps on the main "
                       "stream, join, append, swap"},
            "dense": {"ms_per_block": round(ms_dense, 3),

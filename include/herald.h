@@ -191,6 +191,9 @@ typedef struct {
   const void *q_next;   /* [batch][block][H_q][d] next block's selection queries */
   void *out;            /* step t's output at out + t*out_step_stride     */
   int64_t out_step_stride; /* elements; 0 = every step overwrites out     */
+  int32_t dense;        /* nonzero: this layer keeps exact attention over its
+                           full cache (the paper keeps its first layers so,
+                           sec. IV-B.2); it has no pools and no selection  */
 } herald_layer;
 
 /* Workspace bytes needed by herald_decode_block (0 if invalid). */
@@ -214,7 +217,8 @@ size_t herald_decode_block_workspace(const herald_heads *heads,
  * The caller swaps active and idle for block n+1 (sec. IV-B.1). With dense
  * != 0 the main stream attends over the full cache (rows [0, S_n)) instead of
  * the pool and no selection runs (the GPU-only dense baseline); the append
- * still runs. Everything is ordered on s_main when the call's work ends; the
+ * still runs. A layer whose own dense flag is set is treated so in any case
+ * (its active and idle pools are not read and may be null views). Everything is ordered on s_main when the call's work ends; the
  * retrieval stream first waits for work already enqueued on s_main. k_next
  * (device [batch]) is the next pool's budget; k_max bounds it and
  * k_max + block <= idle.capacity. The cache capacity must hold S_n + block.

@@ -231,15 +231,19 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
   if (num_layers < 1 || batch < 1 || steps < 1 || !layers || !seq_lens || max_seq_len < 1 ||
       max_seq_len > INT32_MAX)
     return HERALD_ERR_INVALID_ARG;
-  if (!dense && (!n_active || max_active < 0 || !n_idle || !k_next || k_max < 1 ||
-                 k_max > max_seq_len))
+  // a layer is dense if the call is (the all-dense baseline) or its own flag is set
+  auto layer_dense = [&](int l) { return dense != 0 || layers[l].dense != 0; };
+  bool any_sparse = false;
+  for (int l = 0; l < num_layers; ++l) any_sparse = any_sparse || !layer_dense(l);
+  if (any_sparse && (!n_active || max_active < 0 || !n_idle || !k_next || k_max < 1 ||
+                     k_max > max_seq_len))
     return HERALD_ERR_INVALID_ARG;
   const int elt = elt_of(heads);
   for (int l = 0; l < num_layers; ++l) {
     const herald_layer &L = layers[l];
     if ((st = check_pool(heads, &L.cache)) != HERALD_OK) return st;
     if ((int64_t)L.cache.capacity < max_seq_len + block) return HERALD_ERR_INVALID_ARG;
-    if (!dense) {
+    if (!layer_dense(l)) {
       if ((st = check_pool(heads, &L.active)) != HERALD_OK) return st;
       if ((st = check_pool(heads, &L.idle)) != HERALD_OK) return st;
       if ((int64_t)L.active.capacity < max_active) return HERALD_ERR_INVALID_ARG;
@@ -252,14 +256,14 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
     if (L.out_step_stride < 0 || !stride_ok(L.out_step_stride, elt)) return HERALD_ERR_INVALID_ARG;
   }
   const size_t need = herald_decode_block_workspace(heads, batch, block, max_seq_len,
-                                                    dense ? 1 : k_max);
+                                                    any_sparse ? k_max : 1);
   if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
 
   // workspace: [selection][idx][attention partials]
   char *w = reinterpret_cast<char *>(ws);
   const size_t sel_bytes = align256(herald_select_workspace(heads, batch, max_seq_len));
   const size_t idx_bytes =
-      align256((size_t)batch * heads->num_kv_heads * (dense ? 1 : k_max) * sizeof(int32_t));
+      align256((size_t)batch * heads->num_kv_heads * (any_sparse ? k_max : 1) * sizeof(int32_t));
   SelectWs sel;
   select_ws_bytes(batch, heads->num_q_heads, heads->num_kv_heads, heads->head_dim, max_seq_len,
                   &sel, w);
@@ -274,11 +278,12 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
   hipError_t e = hipEventCreateWithFlags(&ev_start, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&ev_sel, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventRecord(ev_start, s_main);
-  if (e == hipSuccess && !dense) e = hipStreamWaitEvent(s_retr, ev_start, 0);
+  if (e == hipSuccess && any_sparse) e = hipStreamWaitEvent(s_retr, ev_start, 0);
 
   // retrieval stream: next block's selection + gather into the idle pools
-  if (e == hipSuccess && !dense) {
+  if (e == hipSuccess && any_sparse) {
     for (int l = 0; l < num_layers && e == hipSuccess; ++l) {
+      if (layer_dense(l)) continue;
       const herald_layer &L = layers[l];
       herald_kv cache = kv_of_pool(&L.cache, seq_lens, max_seq_len);
       e = launch_select(*heads, batch, block, L.q_next, view_of(&cache), max_seq_len, k_next,
@@ -293,8 +298,8 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
   for (int t = 0; t < steps && e == hipSuccess; ++t) {
     for (int l = 0; l < num_layers && e == hipSuccess; ++l) {
       const herald_layer &L = layers[l];
-      herald_kv ctx = dense ? kv_of_pool(&L.cache, seq_lens, max_seq_len)
-                            : kv_of_pool(&L.active, n_active, max_active);
+      herald_kv ctx = layer_dense(l) ? kv_of_pool(&L.cache, seq_lens, max_seq_len)
+                                     : kv_of_pool(&L.active, n_active, max_active);
       const char *q = reinterpret_cast<const char *>(L.q_steps) + t * q_step * elt;
       const char *bk = reinterpret_cast<const char *>(L.blk_k) + t * kv_step * elt;
       const char *bv = reinterpret_cast<const char *>(L.blk_v) + t * kv_step * elt;
@@ -304,15 +309,16 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
     }
   }
   // join, append the completed block, advance the lengths
-  if (e == hipSuccess && !dense) e = hipStreamWaitEvent(s_main, ev_sel, 0);
+  if (e == hipSuccess && any_sparse) e = hipStreamWaitEvent(s_main, ev_sel, 0);
   for (int l = 0; l < num_layers && e == hipSuccess; ++l) {
     const herald_layer &L = layers[l];
     const PoolView idle = pool_of(&L.idle);
     e = launch_append(*heads, batch, block, L.done_k, L.done_v, pool_of(&L.cache), seq_lens,
-                      dense ? nullptr : &idle, k_next, k_max, L.cache.capacity, s_main);
+                      layer_dense(l) ? nullptr : &idle, k_next, k_max, L.cache.capacity, s_main);
   }
   if (e == hipSuccess)
-    e = launch_bump(batch, block, seq_lens, dense ? nullptr : n_idle, k_next, k_max, s_main);
+    e = launch_bump(batch, block, seq_lens, any_sparse ? n_idle : nullptr, k_next, k_max,
+                    s_main);
   if (ev_start) hipEventDestroy(ev_start);
   if (ev_sel) hipEventDestroy(ev_sel);
   return hip_status(e);

@@ -40,7 +40,8 @@ class Pool(ctypes.Structure):
 class Layer(ctypes.Structure):
     _fields_ = [("cache", Pool), ("active", Pool), ("idle", Pool), ("q_steps", c_p),
                 ("blk_k", c_p), ("blk_v", c_p), ("done_k", c_p), ("done_v", c_p),
-                ("q_next", c_p), ("out", c_p), ("out_step_stride", c_i64)]
+                ("q_next", c_p), ("out", c_p), ("out_step_stride", c_i64),
+                ("dense", c_i32)]
 
 
 class HeraldError(RuntimeError):

@@ -157,3 +157,28 @@ def test_decode_block_validation():
     assert call(args(kn=None)) == H.ERR_INVALID_ARG
     assert call(args(wsb=10)) == H.ERR_WORKSPACE
     assert call(args(ws=FAKE * 256 + 16)) == H.ERR_WORKSPACE
+
+
+def test_decode_block_dense_layers_need_no_pools():
+    """A layer flagged dense keeps no pools: its null pool views pass the
+    checks, while the sparse layers beside it are still checked."""
+    hd = H.heads(32, 8, 128, "bf16")
+    L = H.lib()
+    cache = H.Pool(FAKE, FAKE, 8 * 2048 * 128, 2048 * 128, 128, 2048)
+    pool = H.Pool(FAKE, FAKE, 8 * 200 * 128, 200 * 128, 128, 200)
+    small = H.Pool(FAKE, FAKE, 8 * 100 * 128, 100 * 128, 128, 100)
+    none = H.Pool(None, None, 0, 0, 0, 0)
+    dense = H.Layer(cache, none, none, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 0, 1)
+
+    def call(layers):
+        arr = (H.Layer * len(layers))(*layers)
+        return L.herald_decode_block(ctypes.byref(hd), len(layers), 2, 32, 4, arr, FAKE, 2000,
+                                     FAKE, 150, FAKE, FAKE, 100, 0, FAKE * 256, 1 << 40,
+                                     None, None)
+    bad = H.Layer(cache, pool, small, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0)
+    good = H.Layer(cache, pool, pool, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0)
+    assert call([dense, bad]) == H.ERR_INVALID_ARG   # idle pool of the sparse layer too small
+    undense = H.Layer(cache, none, none, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 0, 0)
+    assert call([undense, good]) == H.ERR_INVALID_ARG  # same layer without the flag
+    # all checks pass; without a GPU the first HIP call then fails
+    assert call([dense, good]) not in (H.ERR_INVALID_ARG, H.ERR_WORKSPACE)

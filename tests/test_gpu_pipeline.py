@@ -47,7 +47,7 @@ def make_case(b=2, Hq=8, Hkv=2, d=128, B=8, T=2, L=2, nblocks=3, S_lo=900, S_hi=
                 cap=cap, layers=layers)
 
 
-def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20):
+def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, dense_layers=()):
     b, Hq, Hkv, d, B, T, L = (case[x] for x in ("b", "Hq", "Hkv", "d", "B", "T", "L"))
     hd = H.heads(Hq, Hkv, d, "bf16")
     lens_h = case["lens"].copy()
@@ -72,7 +72,9 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20):
     if not dense:
         ws = H.workspace(H.select_workspace(hd, b, int(lens_h.max())), DEV)
         idx = torch.empty((b, Hkv, kmax0), dtype=torch.int32, device=DEV)
-        for lay, L_ in zip(case["layers"], dl):
+        for l, (lay, L_) in enumerate(zip(case["layers"], dl)):
+            if l in dense_layers:
+                continue
             kv = H.kv_view(L_["k"], L_["v"], lens, int(lens_h.max()))
             H.select(hd, b, B, to_dev(lay["q_sel0"]), kv, kps0, kmax0, idx, ws)
             H.gather(hd, b, kv, idx, kps0, kmax0, H.pool_view(*L_["pools"][0]))
@@ -87,13 +89,14 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20):
         kn_h = np.array([H.budget_tokens(int(s), num, den) for s in lens_h], np.int32)
         kn = to_dev(kn_h)
         layers = []
-        for L_ in dl:
+        for l, L_ in enumerate(dl):
             blk = L_["blocks"][n]
             layers.append(H.Layer(
                 H.pool_view(L_["k"], L_["v"]), H.pool_view(*L_["pools"][a]),
                 H.pool_view(*L_["pools"][1 - a]), blk["q"].data_ptr(), blk["bk"].data_ptr(),
                 blk["bv"].data_ptr(), blk["dk"].data_ptr(), blk["dvv"].data_ptr(),
-                blk["qn"].data_ptr(), L_["out"].data_ptr(), b * B * Hq * d))
+                blk["qn"].data_ptr(), L_["out"].data_ptr(), b * B * Hq * d,
+                int(l in dense_layers)))
         torch.cuda.synchronize()
         if delay_main:
             with torch.cuda.stream(s_main):
@@ -111,24 +114,26 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20):
     return outs, caches
 
 
-def oracle_outs(case, num=1, den=20):
-    """Per layer, per sequence: oracle.decode_blocks -> [block][layer][T][b]..."""
+def oracle_outs(case, num=1, den=20, dense_layers=()):
+    """Per layer, per sequence: oracle.decode_blocks -> [block][layer][T][b]...
+    A dense layer is the same schedule at a 100% budget."""
     res = {}
     for l, lay in enumerate(case["layers"]):
+        nm, dn = (1, 1) if l in dense_layers else (num, den)
         for i in range(case["b"]):
             S = int(case["lens"][i])
             K0, V0 = lay["k"][i, :, :S], lay["v"][i, :, :S]
-            k0 = oracle.budget(S, num, den)
+            k0 = oracle.budget(S, nm, dn)
             idx0, _, _, _ = oracle.select(lay["q_sel0"][i], K0, k0)
             blocks = [dict(q_steps=blk["q"][:, i], k_steps=blk["bk"][:, i],
                            v_steps=blk["bv"][:, i], k_done=blk["dk"][i], v_done=blk["dvv"][i],
                            q_next=blk["qn"][i]) for blk in lay["blocks"]]
-            res[(l, i)] = oracle.decode_blocks(K0, V0, idx0, blocks, num, den)
+            res[(l, i)] = oracle.decode_blocks(K0, V0, idx0, blocks, nm, dn)
     return res
 
 
-def check_against_oracle(case, outs, num=1, den=20):
-    ref = oracle_outs(case, num, den)
+def check_against_oracle(case, outs, num=1, den=20, dense_layers=()):
+    ref = oracle_outs(case, num, den, dense_layers)
     worst = 0.0
     for n in range(case["nblocks"]):
         for l in range(case["L"]):
@@ -168,6 +173,15 @@ def test_dense_mode_matches_full_budget_oracle():
     case = make_case(seed=3, nblocks=2)
     outs, _ = run_gpu(case, dense=True)
     check_against_oracle(case, outs, num=1, den=1)
+
+
+def test_pipeline_with_dense_first_layers():
+    """Layers flagged dense keep exact attention over the growing cache (the
+    oracle's schedule at a 100% budget) while the sparse layers beside them
+    follow the 5% schedule; layer 0 dense, layers 1-2 sparse."""
+    case = make_case(seed=5, L=3)
+    outs, _ = run_gpu(case, dense_layers=(0,))
+    check_against_oracle(case, outs, dense_layers=(0,))
 
 
 def test_pipeline_layer32k_shapes_one_block():
