@@ -4,12 +4,13 @@
 // Four launches per call, all on the caller's stream:
 //   repq   : qbar[b][h][e][g] = mean over the B block queries (fp64), and
 //            clears the first-level histogram.
-//   score  : one workgroup per (chunk of 1024 cached rows, KV head, sequence).
-//            Streams K once with coalesced 128-bit non-temporal loads, turns
-//            the tile around in LDS so that each lane owns one row, and forms
-//            the G raw scores of that row with fp64 FMAs whose qbar operand
-//            comes from scalar registers. Writes the scores z (fp64) and the
-//            chunk's softmax statistics (max, sum of exp).
+//   score  : one workgroup per (chunk of 2048 cached rows, KV head, sequence).
+//            Streams K once with coalesced 128-bit non-temporal loads and
+//            forms the G raw scores of every row in fp64: on the fp64 matrix
+//            cores for G <= 4 (each wave stages its tiles through its own LDS
+//            region into the MFMA operand layout), with fp64 FMAs for G = 8.
+//            Writes the scores z (fp64) and the chunk's softmax statistics
+//            (max, sum of exp).
 //   norm   : merges the chunk statistics into (m_g, l_g), forms the GQA
 //            importance s_hat = sum_g exp(z_g - m_g) / l_g (fp64), stores its
 //            bit pattern as a 64-bit ranking key, and histograms the key's
@@ -78,8 +79,8 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
   for (int t = threadIdx.x; t < kHistBins; t += 256) hist[bh * kHistBins + t] = 0u;
 }
 
-// ---------------------------------------------------------------- score
-// Workgroup = 2 wave pairs. A pair scores one 64-row tile at a time: both
+// ---------------------------------------------------------------- score (FMA)
+// Used for G = 8. Workgroup = 2 wave pairs. A pair scores one 64-row tile at a time: both
 // waves stage the tile (coalesced 1 KiB loads) into LDS, then each lane owns
 // one row and each wave of the pair forms the partial dot products of one
 // half of the head dimension with the qbar half it holds in scalar registers.
@@ -248,6 +249,178 @@ __global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
     double *p = part + ((bh * nchunk + chunk) * G + g) * 2;
     p[0] = fmax(red[half][gg], red[half + 2][gg]);
     p[1] = red2[half][gg] + red2[half + 2][gg];
+  }
+}
+
+// ---------------------------------------------------------------- score (MFMA)
+// The dot products run on the fp64 matrix cores: v_mfma_f64_4x4x4_4b forms
+// four independent 4x4x4 products per instruction. Each of its blocks takes
+// four cached rows (A: 4 rows x 4 head-dim elements) against the same qbar
+// slice (B: 4 elements x the query heads of the group, zero past G), so a
+// chain of D/4 instructions scores 16 rows for all G heads, every multiply
+// useful when G = 4. Operand layout: A lane l holds row l % 16 at element
+// slot l / 16, B lane l holds slot l / 16 of head l % 4, and the result of
+// lane l is row 4 ((l / 4) % 4) + l / 16, head l % 4. The head dimension is
+// enumerated in the same permuted order on both operands (a sum does not
+// depend on it beyond rounding) so that a lane reads whole 16-byte pieces of
+// its row. Two accumulators per 16 rows (first and second half of the
+// elements, added in that order) and up to four 16-row chains per tile keep
+// independent chains in flight.
+// Each wave scores its own 8 KiB tiles (64, 32 or 16 rows of 128, 256 or 512
+// bytes): coalesced 1 KiB loads into a
+// wave-private LDS region, read back in the operand layout; the next tile's
+// loads are in flight while the current one is multiplied. The only
+// workgroup barriers merge the chunk statistics at the end.
+template <int D, int G, bool BF16, bool PAGED>
+__global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
+                                                            const double *__restrict__ qbar,
+                                                            double *__restrict__ zspill,
+                                                            double *__restrict__ part,
+                                                            int Hkv, int64_t S_pad,
+                                                            int nchunk, double scale) {
+  static_assert(G <= 4, "one MFMA column per query head of the group");
+  constexpr int ELT = BF16 ? 2 : 4;
+  constexpr int RB = D * ELT;                   // bytes per cached row
+  constexpr int EPP = 16 / ELT;                 // elements per 16-byte piece
+  constexpr int NP = RB / 64;                   // pieces per lane and row (4 lanes per row)
+  constexpr int NS = D / 4;                     // MFMA steps over the head dimension
+  constexpr int NH = NS / 2;                    // steps per accumulator
+  constexpr int WR = 8192 / RB;                 // rows per wave tile
+  constexpr int NC = WR / 16;                   // 16-row chains per tile
+  constexpr int RPL = 1024 / RB;                // rows per wave-wide 1 KiB load
+  constexpr int LPR = RB / 16;                  // lanes per row in such a load
+  constexpr int NLD = WR / RPL;                 // loads per lane and tile
+  constexpr int LSTR = RB + 16;                 // padded LDS row stride
+  constexpr int NW = 4;                         // waves per workgroup
+  constexpr int TPW = kScoreChunk / (WR * NW);  // tiles per wave
+  static_assert(NP * EPP == NS && NS % 2 == 0, "head dimension split");
+  __shared__ __attribute__((aligned(16))) char lds[NW][WR * LSTR];
+  __shared__ double red[NW][4], red2[NW][4];
+
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = kv_len(kv, b);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S) return;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  char *my = lds[wave];
+  const int kq = lane >> 4;                               // element slot (A and B)
+  const int g = lane & 3;                                 // head (B column, result)
+  const int zrow = 4 * ((lane >> 2) & 3) + (lane >> 4);   // result row within 16
+
+  // B operand of every step: qbar at the permuted element, zero past G
+  double bq[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int e = (s / EPP) * (4 * EPP) + kq * EPP + s % EPP;
+    const double q = qbar[(bh * D + e) * G + (g < G ? g : G - 1)];
+    bq[s] = g < G ? q : 0.0;
+  }
+
+  const int lr = lane / LPR, lc = lane % LPR;
+  const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + lc * 16;
+  // row s of a load whose first row s_base is uniform (a load never crosses
+  // a page: pages hold at least 8 rows and loads start at multiples of RPL)
+  auto row_addr = [&](int64_t s_base, int64_t s) -> const char * {
+    if (PAGED) {
+      const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s_base >> kv.page_shift)];
+      return kv.k + (page * kv.sp + (int64_t)h * kv.sh +
+                     (s & ((1 << kv.page_shift) - 1)) * kv.ss) * ELT + lc * 16;
+    }
+    return kbase + s * kv.ss * ELT;
+  };
+  // the waves take interleaved tiles, so that together they stream the chunk
+  auto tile_row0 = [&](int t) { return c0 + (int64_t)(t * NW + wave) * WR; };
+  uint4 buf[NLD];
+  auto load_tile = [&](int t) {
+    const int64_t r0 = tile_row0(t);
+    if (r0 + WR <= S) {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) buf[i] = ldg16_nt(row_addr(r0 + i * RPL, r0 + i * RPL + lr));
+    } else {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const int64_t s = r0 + i * RPL + lr;
+        buf[i] = make_uint4(0u, 0u, 0u, 0u);
+        if (s < S) buf[i] = ldg16_nt(row_addr(r0 + i * RPL, s));
+      }
+    }
+  };
+
+  double m_l = -INFINITY, l_l = 0.0;
+  load_tile(0);
+#pragma unroll 1
+  for (int t = 0; t < TPW; ++t) {
+    const int64_t r0 = tile_row0(t);
+    if (r0 >= S) break;  // uniform: later tiles of this wave start later still
+#pragma unroll
+    for (int i = 0; i < NLD; ++i)
+      *reinterpret_cast<uint4 *>(my + (i * RPL + lr) * LSTR + lc * 16) = buf[i];
+    // the wave's LDS operations complete in order: the reads below see the
+    // writes above, and the next tile's writes follow these reads
+    asm volatile("" ::: "memory");
+    uint4 a[NC][NP];
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+        a[c][p] = *reinterpret_cast<const uint4 *>(my + (16 * c + (lane & 15)) * LSTR + p * 64 +
+                                                   kq * 16);
+    asm volatile("" ::: "memory");
+    if (t + 1 < TPW && tile_row0(t + 1) < S) load_tile(t + 1);
+
+    auto elem = [&](const uint4 *pc, int s) -> double {
+      const uint4 v = pc[s / EPP];
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+      const int e = s % EPP;
+      if (BF16) return (double)((e & 1) ? bf16_hi(w[e >> 1]) : bf16_lo(w[e >> 1]));
+      return (double)__uint_as_float(w[e]);
+    };
+    double acc[NC][2];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c][0] = acc[c][1] = 0.0;
+#pragma unroll
+    for (int s = 0; s < NH; ++s)
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          acc[c][hh] = __builtin_amdgcn_mfma_f64_4x4x4f64(elem(a[c], s + hh * NH),
+                                                          bq[s + hh * NH], acc[c][hh], 0, 0, 0);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int64_t s = r0 + 16 * c + zrow;
+      if (g < G && s < S) {
+        const double z = (acc[c][0] + acc[c][1]) * scale;
+        zspill[(bh * S_pad + s) * G + g] = z;
+        // one exp per score: exp(-|z - m|) either rescales the old sum or is
+        // the new term
+        const double dz = z - m_l;
+        const double e = exp(-fabs(dz));
+        const bool up = dz > 0.0;
+        l_l = up ? fma(l_l, e, 1.0) : l_l + e;
+        m_l = up ? z : m_l;
+      }
+    }
+  }
+
+  // chunk statistics of head g: max over the 16 lanes of g in each wave and
+  // over the waves, then the rescaled sums in the same order
+  double m = m_l;
+#pragma unroll
+  for (int off = 4; off <= 32; off <<= 1) m = fmax(m, __shfl_xor(m, off, 64));
+  if (lane < 4) red[wave][lane] = m;
+  __syncthreads();
+  const double mc = fmax(fmax(red[0][g], red[1][g]), fmax(red[2][g], red[3][g]));
+  double v = m_l == -INFINITY ? 0.0 : l_l * exp(m_l - mc);
+#pragma unroll
+  for (int off = 4; off <= 32; off <<= 1) v += __shfl_xor(v, off, 64);
+  if (lane < 4) red2[wave][lane] = v;
+  __syncthreads();
+  if (wave == 0 && lane < G) {
+    double *p = part + ((bh * nchunk + chunk) * G + lane) * 2;
+    p[0] = mc;
+    p[1] = ((red2[0][lane] + red2[1][lane]) + red2[2][lane]) + red2[3][lane];
   }
 }
 
@@ -529,12 +702,21 @@ hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView
   repq_kernel<D, G, BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist,
                                                                  block, Hq, Hkv);
   const dim3 grid(ws.nchunk, Hkv, batch);
-  if (kv.pt)
-    score_kernel<D, G, BF16, true><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
-                                                             Hkv, ws.S_pad, ws.nchunk, scale);
-  else
-    score_kernel<D, G, BF16, false><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
-                                                              Hkv, ws.S_pad, ws.nchunk, scale);
+  if constexpr (G <= 4) {
+    if (kv.pt)
+      score_mfma_kernel<D, G, BF16, true><<<grid, 256, 0, stream>>>(
+          kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+    else
+      score_mfma_kernel<D, G, BF16, false><<<grid, 256, 0, stream>>>(
+          kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+  } else {
+    if (kv.pt)
+      score_kernel<D, G, BF16, true><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
+                                                               Hkv, ws.S_pad, ws.nchunk, scale);
+    else
+      score_kernel<D, G, BF16, false><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
+                                                                Hkv, ws.S_pad, ws.nchunk, scale);
+  }
   norm_kernel<G><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist,
                                            Hkv, ws.S_pad, ws.nchunk, kv.max_len);
   topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
