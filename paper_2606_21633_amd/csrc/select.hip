@@ -2,8 +2,8 @@
 // importance and per-KV-head top-k (sec. IV-A.2 and sec. IV-B.4 of the paper).
 //
 // Four launches per call, all on the caller's stream:
-//   repq   : qbar[b][h][e][g] = mean over the B block queries (fp64), and
-//            clears the first-level histogram.
+//   repq   : qbar[b][h][e][g] = mean over the B block queries (fp64), one
+//            (element, head) per thread, and clears the first-level histogram.
 //   score  : one workgroup per (chunk of 2048 cached rows, KV head, sequence).
 //            Streams K once with coalesced 128-bit non-temporal loads and
 //            forms the G raw scores of every row in fp64: on the fp64 matrix
@@ -30,8 +30,9 @@ namespace herald {
 namespace {
 
 constexpr int kTopkThreads = 1024;
-constexpr int kCandCap = 8192;
-constexpr int kEmitPerThread = 8;
+constexpr int kCandCap = 16384;  // LDS candidates (128 KiB of keys)
+constexpr int kEmitPerThread = 16;  // consecutive keys per thread in the emission
+constexpr int kKeysPerThread = 16;  // keys per thread and round in the passes over S
 
 // (m, l) <- softmax-statistics merge of (m, l) and (m2, l2).
 __device__ __forceinline__ void merge_ml(double &m, double &l, double m2, double l2) {
@@ -50,7 +51,9 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
   constexpr int U = 64;  // loads in flight per thread: every block row at once
   const int h = blockIdx.x, b = blockIdx.y;
   const int64_t bh = (int64_t)b * Hkv + h;
-  for (int t = threadIdx.x; t < D * G; t += 256) {
+  // one (element, head) per thread; blockIdx.z covers the D * G of them
+  const int t = blockIdx.z * 256 + threadIdx.x;
+  if (t < D * G) {
     const int e = t % D, g = t / D;
     const int hq = h * G + g;
     const int64_t base = ((int64_t)b * block * Hq + hq) * D + e;
@@ -76,7 +79,8 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
     }
     qbar[(bh * D + e) * G + g] = acc / (double)block;
   }
-  for (int t = threadIdx.x; t < kHistBins; t += 256) hist[bh * kHistBins + t] = 0u;
+  if (blockIdx.z == 0)
+    for (int i = threadIdx.x; i < kHistBins; i += 256) hist[bh * kHistBins + i] = 0u;
 }
 
 // ---------------------------------------------------------------- score (FMA)
@@ -519,35 +523,30 @@ __device__ __forceinline__ int block_excl_scan(int v, int *wsum, int *total) {
   return before + incl - v;
 }
 
-// Wave 0 finds the digit d with above(d) < r <= above(d) + cnt[d], where
-// above(d) counts keys in bins > d. Results go to shared memory.
-__device__ __forceinline__ void find_digit(const uint32_t *cnt, int nbins, int r,
+// All threads: the digit d with above(d) < r <= above(d) + cnt[d], where
+// above(d) counts keys in bins > d. Thread t sums the bins at ranks
+// [per t, per (t + 1)) from the top; a block scan of those sums locates the
+// one thread whose bins hold rank r. Results go to shared memory.
+__device__ __forceinline__ void find_digit(const uint32_t *cnt, int nbins, int r, int *wsum,
                                            int *s_digit, int *s_above, int *s_cnt) {
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    const int per = (nbins + 63) / 64;          // bins per lane, from the top
-    const int hi = nbins - per * lane;           // lane covers [hi - per, hi)
-    int mine = 0;
+  const int tid = threadIdx.x;
+  const int per = nbins > kTopkThreads ? nbins / kTopkThreads : 1;  // nbins: power of two
+  const int hi = nbins - per * tid;                                 // bins [hi - per, hi)
+  int mine = 0;
+  for (int i = 0; i < per; ++i) {
+    const int bin = hi - 1 - i;
+    if (bin >= 0) mine += (int)cnt[bin];
+  }
+  int total;
+  const int before = block_excl_scan(mine, wsum, &total);
+  if (before < r && r <= before + mine) {
+    int acc = before;
     for (int i = 0; i < per; ++i) {
       const int bin = hi - 1 - i;
-      if (bin >= 0) mine += (int)cnt[bin];
-    }
-    int incl = mine;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += y;
-    }
-    const int before = incl - mine;
-    if (before < r && r <= incl) {
-      int acc = before;
-      for (int i = 0; i < per; ++i) {
-        const int bin = hi - 1 - i;
-        if (bin < 0) break;
-        const int c = (int)cnt[bin];
-        if (acc + c >= r) { *s_digit = bin; *s_above = acc; *s_cnt = c; break; }
-        acc += c;
-      }
+      if (bin < 0) break;
+      const int c = (int)cnt[bin];
+      if (acc + c >= r) { *s_digit = bin; *s_above = acc; *s_cnt = c; break; }
+      acc += c;
     }
   }
   __syncthreads();
@@ -557,6 +556,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     const int32_t *__restrict__ lens, const int32_t *__restrict__ kps, int k_max,
     const uint64_t *__restrict__ keys, const uint32_t *__restrict__ hist,
     int32_t *__restrict__ idx_out, int Hkv, int64_t S_pad, int64_t max_len) {
+  constexpr int KPT = kKeysPerThread;
   __shared__ uint32_t cnt[kHistBins];
   __shared__ uint64_t cand[kCandCap];
   __shared__ int wsum[kTopkThreads / 64];
@@ -564,11 +564,12 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
 
   const int h = blockIdx.x, b = blockIdx.y;
   const int64_t bh = (int64_t)b * Hkv + h;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
   const int k = clamp_k(kps[b], S, k_max);
   int32_t *out = idx_out + bh * k_max;
   const uint64_t *kb = keys + bh * S_pad;
+  const uint64_t lanes_below = (1ull << lane) - 1ull;
 
   if (k == 0 || k == S) {
     for (int j = tid; j < k_max; j += kTopkThreads) out[j] = j < k ? j : -1;
@@ -578,7 +579,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   for (int i = tid; i < kHistBins; i += kTopkThreads) cnt[i] = hist[bh * kHistBins + i];
   if (tid == 0) s_ncand = 0;
   __syncthreads();
-  find_digit(cnt, kHistBins, k, &s_digit, &s_above, &s_cnt);
+  find_digit(cnt, kHistBins, k, wsum, &s_digit, &s_above, &s_cnt);
   uint64_t P = (uint64_t)s_digit;
   int r = k - s_above;
   int c = s_cnt;
@@ -586,28 +587,34 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   bool in_lds = false;
   int ncand = 0;
 
-  // compact the keys whose top (64 - L) bits equal P into LDS
+  // compact the keys whose top (64 - L) bits equal P into LDS: KPT keys per
+  // thread in flight, one slot reservation per wave and round
   auto compact = [&]() {
-    for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * 8) {
-      uint64_t key[8];
+    for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * KPT) {
+      uint64_t key[KPT];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < KPT; ++u) {
         const int64_t s = base + (int64_t)u * kTopkThreads + tid;
         key[u] = s < S ? kb[s] : 0;
       }
+      uint64_t bal[KPT];
+      int n = 0;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < KPT; ++u) {
         const int64_t s = base + (int64_t)u * kTopkThreads + tid;
-        const bool match = s < S && (key[u] >> L) == P;
-        const uint64_t bal = __ballot(match);
-        int slot0 = 0;
-        const int lane = tid & 63;
-        if (lane == 0 && bal) slot0 = atomicAdd(&s_ncand, __popcll(bal));
-        slot0 = __shfl(slot0, 0, 64);
-        if (match) {
-          const int slot = slot0 + __popcll(bal & ((1ull << lane) - 1ull));
-          if (slot < kCandCap) cand[slot] = key[u];
+        bal[u] = __ballot(s < S && (key[u] >> L) == P);
+        n += __popcll(bal[u]);
+      }
+      int slot = 0;
+      if (lane == 0 && n) slot = atomicAdd(&s_ncand, n);
+      slot = __shfl(slot, 0, 64);
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) {
+        if ((bal[u] >> lane) & 1ull) {
+          const int at = slot + __popcll(bal[u] & lanes_below);
+          if (at < kCandCap) cand[at] = key[u];
         }
+        slot += __popcll(bal[u]);
       }
     }
     __syncthreads();
@@ -628,21 +635,21 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
         if ((key >> L) == P) atomicAdd(&cnt[(uint32_t)(key >> L2) & mask], 1u);
       }
     } else {
-      for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * 8) {
-        uint64_t key[8];
+      for (int64_t base = 0; base < S; base += (int64_t)kTopkThreads * KPT) {
+        uint64_t key[KPT];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < KPT; ++u) {
           const int64_t s = base + (int64_t)u * kTopkThreads + tid;
           key[u] = s < S ? kb[s] : ~0ull;
         }
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < KPT; ++u)
           if (base + (int64_t)u * kTopkThreads + tid < S && (key[u] >> L) == P)
             atomicAdd(&cnt[(uint32_t)(key[u] >> L2) & mask], 1u);
       }
     }
     __syncthreads();
-    find_digit(cnt, 1 << nb, r, &s_digit, &s_above, &s_cnt);
+    find_digit(cnt, 1 << nb, r, wsum, &s_digit, &s_above, &s_cnt);
     r -= s_above;
     P = (P << nb) | (uint64_t)s_digit;
     c = s_cnt;
@@ -651,44 +658,57 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     if (!in_lds && c != r && c <= kCandCap) compact();
   }
 
-  // Ordered emission: keys above the boundary bucket always, bucket members
-  // (equal top bits; exact ties once L == 0) lowest index first, r of them.
+  // Ordered emission: keys above the boundary bucket always; bucket members
+  // (equal top bits; exact ties once L == 0) all of them when the bucket holds
+  // exactly r keys, else the r of lowest index. Each thread takes E
+  // consecutive indices, so a block scan of the per-thread counts gives the
+  // output positions in ascending index order.
+  constexpr int E = kEmitPerThread;
+  const bool whole_bucket = c == r;
   int base_eq = 0, base_sel = 0;
-  for (int64_t t0 = 0; t0 < S; t0 += (int64_t)kTopkThreads * kEmitPerThread) {
-    const int64_t s0 = t0 + (int64_t)tid * kEmitPerThread;
-    bool gt[kEmitPerThread], eq[kEmitPerThread];
-    int n_eq = 0;
-    uint64_t key[kEmitPerThread];
+  for (int64_t t0 = 0; t0 < S; t0 += (int64_t)kTopkThreads * E) {
+    const int64_t s0 = t0 + (int64_t)tid * E;
+    uint64_t key[E];
+    if (s0 + E <= S) {
 #pragma unroll
-    for (int u = 0; u < kEmitPerThread; ++u) key[u] = s0 + u < S ? kb[s0 + u] : 0;
+      for (int j = 0; j < E / 2; ++j) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(kb + s0 + 2 * j);
+        key[2 * j] = (uint64_t)v.x | ((uint64_t)v.y << 32);
+        key[2 * j + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
+      }
+    } else {
 #pragma unroll
-    for (int u = 0; u < kEmitPerThread; ++u) {
-      const int64_t s = s0 + u;
-      const bool valid = s < S;
-      const uint64_t hi = valid ? (key[u] >> L) : 0;
-      gt[u] = valid && hi > P;
-      eq[u] = valid && hi == P;
-      n_eq += eq[u];
+      for (int u = 0; u < E; ++u) key[u] = s0 + u < S ? kb[s0 + u] : 0;
     }
-    int tot_eq;
-    int rank = base_eq + block_excl_scan(n_eq, wsum, &tot_eq);
-    bool take[kEmitPerThread];
-    int n_take = 0;
+    uint32_t gt = 0, eq = 0;
 #pragma unroll
-    for (int u = 0; u < kEmitPerThread; ++u) {
-      take[u] = gt[u] || (eq[u] && rank < r);
-      rank += eq[u];
-      n_take += take[u];
+    for (int u = 0; u < E; ++u) {
+      const bool valid = s0 + u < S;
+      const uint64_t hi = valid ? (key[u] >> L) : 0;
+      gt |= (uint32_t)(valid && hi > P) << u;
+      eq |= (uint32_t)(valid && hi == P) << u;
+    }
+    uint32_t take = gt | eq;
+    if (!whole_bucket) {
+      int tot_eq;
+      int rank = base_eq + block_excl_scan(__popc(eq), wsum, &tot_eq);
+      take = gt;
+#pragma unroll
+      for (int u = 0; u < E; ++u)
+        if ((eq >> u) & 1u) {
+          if (rank < r) take |= 1u << u;
+          ++rank;
+        }
+      base_eq += tot_eq;
     }
     int tot_take;
-    int pos = base_sel + block_excl_scan(n_take, wsum, &tot_take);
+    int pos = base_sel + block_excl_scan(__popc(take), wsum, &tot_take);
 #pragma unroll
-    for (int u = 0; u < kEmitPerThread; ++u)
-      if (take[u]) {
+    for (int u = 0; u < E; ++u)
+      if ((take >> u) & 1u) {
         if (pos < k) out[pos] = (int32_t)(s0 + u);  // counts are exact; guard anyway
         ++pos;
       }
-    base_eq += tot_eq;
     base_sel += tot_take;
   }
   for (int j = k + tid; j < k_max; j += kTopkThreads) out[j] = -1;
@@ -699,8 +719,8 @@ hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView
                            int Hq, int Hkv, const int32_t *k_per_seq, int k_max,
                            int32_t *idx_out, const SelectWs &ws, hipStream_t stream) {
   const double scale = 1.0 / sqrt((double)D);
-  repq_kernel<D, G, BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist,
-                                                                 block, Hq, Hkv);
+  repq_kernel<D, G, BF16><<<dim3(Hkv, batch, (D * G + 255) / 256), 256, 0, stream>>>(
+      q_sel, ws.qbar, ws.hist, block, Hq, Hkv);
   const dim3 grid(ws.nchunk, Hkv, batch);
   if constexpr (G <= 4) {
     if (kv.pt)

@@ -96,6 +96,18 @@ def test_select_exact_ties_go_to_lower_index(kk):
     np.testing.assert_array_equal(got[0, 0], np.arange(kk))
 
 
+@pytest.mark.parametrize("kk", [1, 9999, 19999])
+def test_select_exact_ties_beyond_lds_candidates(kk):
+    # 20000 identical keys: the boundary bucket exceeds the 16384 candidates
+    # the top-k kernel holds in LDS, so every digit is resolved by passes over
+    # the keys in global memory, down to the exact tie
+    wl, inp = _tie_inputs(S=20000)
+    assert check_select(wl, inp, np.array([kk, kk]), kk) == 0
+    st = Staged(wl, inp)
+    got, _ = st.select(np.array([kk, kk], np.int32), kk)
+    np.testing.assert_array_equal(got[0, 0], np.arange(kk))
+
+
 @pytest.mark.parametrize("pos", [0, 3, 63, 64, 1023, 1024, 2047, 4095, 4096, 4999])
 def test_select_dominant_key_found_anywhere(pos):
     wl = SMALL.replace(name="dominant", batch=1, seq_len=5000, seq_len_lo=0, seed=pos)
