@@ -17,6 +17,13 @@ Functions and the passages of the paper they follow:
                   statistics per query head, GQA importance
                   s_hat_h[s] = sum_g exp(s[g,s]-m_g)/l_g and one top-k per
                   KV head (sec. IV-B.4). Ties: lower index; output ascending.
+* ``select_xq``   selection with x query rows used as they are: the x rows
+                  centred in the block (rows floor((B-x)/2) ...), softmax
+                  statistics per (row, head) and the importance summed over
+                  all x*G softmax-normalised score rows (the G-sum of
+                  sec. IV-B.4 extended over rows, a reading). x = 1 is the
+                  centre [MASK] query of sec. IV-A.2 (Eq. 2; lower middle
+                  row for even B); x = B every query of the block.
 * ``gather``      copy of the selected rows into the sparse pool (sec. IV-B.3).
 * ``attn``        B-query GQA attention over a context plus the block's own
                   KV, unmasked (sec. II-A: bidirectional inside the block,
@@ -67,6 +74,9 @@ def _load():
     lib.herald_oracle_select.restype = i32
     lib.herald_oracle_select.argtypes = [i32, i32, i32, i32, i64, p, i32, p, i32,
                                          i64, p, p, p, p]
+    lib.herald_oracle_select_xq.restype = i32
+    lib.herald_oracle_select_xq.argtypes = [i32, i32, i32, i32, i32, i64, p, i32, p, i32,
+                                            i64, p, p]
     lib.herald_oracle_gather.restype = i32
     lib.herald_oracle_gather.argtypes = [i32, i32, i64, p, i32, p, i64, i64, p]
     lib.herald_oracle_attn.restype = i32
@@ -131,6 +141,25 @@ def select(q_sel, K, k: int):
     if rc != 0:
         raise ValueError("herald_oracle_select: bad arguments")
     return idx, s_hat, m, l
+
+
+def select_xq(q_sel, K, k: int, x: int):
+    """One sequence, x query rows. q_sel [B][Hq][d], K [Hkv][S][d].
+
+    Returns (idx int32 [Hkv][k] ascending, s_hat float64 [Hkv][S]).
+    """
+    q, qt = _as_np(q_sel)
+    kk, kt = _as_np(K)
+    B, Hq, d = q.shape
+    Hkv, S, d2 = kk.shape
+    assert d == d2 and Hq % Hkv == 0
+    idx = np.empty((Hkv, k), np.int32)
+    s_hat = np.empty((Hkv, S), np.float64)
+    rc = _load().herald_oracle_select_xq(B, int(x), Hq, Hkv, d, S, _ptr(q), qt, _ptr(kk), kt,
+                                         int(k), _ptr(s_hat), _ptr(idx))
+    if rc != 0:
+        raise ValueError("herald_oracle_select_xq: bad arguments")
+    return idx, s_hat
 
 
 def gather(K, idx, cap: int | None = None):

@@ -20,6 +20,19 @@
  *                          s_hat_h[s] = sum_g exp(s[g,s]-m_g)/l_g followed by
  *                          one top-k per KV head (sec. IV-B.4). Ties go to the
  *                          lower index; the output is in ascending index order.
+ *   herald_oracle_select_xq
+ *                          selection with x query rows of the block used as
+ *                          they are: the x rows centred in the block, rows
+ *                          floor((B-x)/2) .. floor((B-x)/2)+x-1, each with its
+ *                          own softmax statistics per query head, and the
+ *                          importance summed over all x*G softmax-normalised
+ *                          score rows (the G-sum of sec. IV-B.4 extended over
+ *                          query rows; the paper gives no rule for x > 1, this
+ *                          is a reading). x = 1 is the centre [MASK] query of
+ *                          sec. IV-A.2 (Eq. 2 is minimised by the row nearest
+ *                          the block centre; for even B the two middle rows
+ *                          tie and the lower is taken); x = B uses every
+ *                          query of the block. Same top-k and tie rule.
  *   herald_oracle_gather   copy of the selected K/V rows into a dense pool
  *                          (sec. IV-B.3, the gather of the selected entries).
  *   herald_oracle_attn     B-query GQA attention of a block over a context
@@ -78,6 +91,14 @@ static int cmp_rank(const void *a, const void *b) {
 static int cmp_i32(const void *a, const void *b) {
   int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
   return (x > y) - (x < y);
+}
+
+/* one top-k per KV head: the first k under (importance desc, index asc),
+ * written in ascending index order */
+static void topk_ascending(ranked *r, int64_t S, int64_t k, int32_t *out) {
+  qsort(r, (size_t)S, sizeof(ranked), cmp_rank);
+  for (int64_t j = 0; j < k; ++j) out[j] = (int32_t)r[j].idx;
+  qsort(out, (size_t)k, sizeof(int32_t), cmp_i32);
 }
 
 /*
@@ -148,12 +169,73 @@ int herald_oracle_select(int B, int Hq, int Hkv, int d, int64_t S,
       r[s].idx = s;
       if (s_hat_out) s_hat_out[(int64_t)h * S + s] = acc;
     }
-    /* one top-k per KV head: the first k under (importance desc, index asc) */
-    qsort(r, (size_t)S, sizeof(ranked), cmp_rank);
-    int32_t *out = idx_out + (int64_t)h * k;
-    for (int64_t j = 0; j < k; ++j) out[j] = (int32_t)r[j].idx;
-    qsort(out, (size_t)k, sizeof(int32_t), cmp_i32);
+    topk_ascending(r, S, k, idx_out + (int64_t)h * k);
     free(qbar); free(z); free(m); free(l); free(r);
+  }
+  return fail ? -1 : 0;
+}
+
+/*
+ * One sequence, x query rows. Shapes as herald_oracle_select; 1 <= x <= B.
+ * Writes s_hat [Hkv][S] (if non-NULL) and idx [Hkv][k] (ascending).
+ */
+int herald_oracle_select_xq(int B, int x, int Hq, int Hkv, int d, int64_t S,
+                            const void *q_sel, int q_type, const void *K,
+                            int k_type, int64_t k, double *s_hat_out,
+                            int32_t *idx_out) {
+  if (B < 1 || x < 1 || x > B || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 ||
+      S < 1 || k < 1 || k > S)
+    return -1;
+  const int G = Hq / Hkv;
+  const int c0 = (B - x) / 2; /* first row of the centred window */
+  const int V = x * G;        /* score rows: query row i, head g -> v = i*G+g */
+  const double scale = 1.0 / sqrt((double)d);
+  int fail = 0;
+
+#pragma omp parallel for schedule(dynamic) reduction(| : fail)
+  for (int h = 0; h < Hkv; ++h) {
+    double *z = (double *)malloc(sizeof(double) * (size_t)V * S);
+    double *m = (double *)malloc(sizeof(double) * V);
+    double *l = (double *)malloc(sizeof(double) * V);
+    ranked *r = (ranked *)malloc(sizeof(ranked) * (size_t)S);
+    if (!z || !m || !l || !r) {
+      fail = 1;
+      free(z); free(m); free(l); free(r);
+      continue;
+    }
+    /* raw scores of every window row and head over every prefix entry */
+    for (int i = 0; i < x; ++i)
+      for (int g = 0; g < G; ++g) {
+        const int v = i * G + g, hq = h * G + g;
+        const int64_t q0 = ((int64_t)(c0 + i) * Hq + hq) * d;
+        for (int64_t s = 0; s < S; ++s) {
+          double acc = 0.0;
+          for (int e = 0; e < d; ++e)
+            acc += load_elem(q_sel, q_type, q0 + e) *
+                   load_elem(K, k_type, ((int64_t)h * S + s) * d + e);
+          z[(int64_t)v * S + s] = acc * scale;
+        }
+      }
+    /* softmax statistics of every score row */
+    for (int v = 0; v < V; ++v) {
+      double mx = -INFINITY;
+      for (int64_t s = 0; s < S; ++s)
+        if (z[(int64_t)v * S + s] > mx) mx = z[(int64_t)v * S + s];
+      double sum = 0.0;
+      for (int64_t s = 0; s < S; ++s) sum += exp(z[(int64_t)v * S + s] - mx);
+      m[v] = mx;
+      l[v] = sum;
+    }
+    /* importance: sum over the x*G softmax-normalised score rows */
+    for (int64_t s = 0; s < S; ++s) {
+      double acc = 0.0;
+      for (int v = 0; v < V; ++v) acc += exp(z[(int64_t)v * S + s] - m[v]) / l[v];
+      r[s].key = acc;
+      r[s].idx = s;
+      if (s_hat_out) s_hat_out[(int64_t)h * S + s] = acc;
+    }
+    topk_ascending(r, S, k, idx_out + (int64_t)h * k);
+    free(z); free(m); free(l); free(r);
   }
   return fail ? -1 : 0;
 }

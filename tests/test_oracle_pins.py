@@ -197,6 +197,107 @@ def test_ties_go_to_lower_index():
     np.testing.assert_array_equal(idx[0], np.arange(7))
 
 
+# ---------------------------------------------------------------- x query rows
+
+
+def _mp_select_xq(q_sel, K, k, rows):
+    """50-digit brute force of the x-row selection over the given block rows:
+    per (row, head) scores and softmax, summed over rows and the group."""
+    mpmath.mp.dps = 50
+    q = _f64(q_sel)
+    kk = _f64(K)
+    _, Hq, d = q.shape
+    Hkv, S, _ = kk.shape
+    G = Hq // Hkv
+    scale = 1 / mpmath.sqrt(d)
+    shat = [[mpmath.mpf(0)] * S for _ in range(Hkv)]
+    for i in rows:
+        for hq in range(Hq):
+            h = hq // G
+            z = [scale * mpmath.fsum(mpmath.mpf(float(q[i, hq, e])) * mpmath.mpf(float(kk[h, s, e]))
+                                     for e in range(d)) for s in range(S)]
+            den = mpmath.fsum(mpmath.exp(x) for x in z)
+            for s in range(S):
+                shat[h][s] += mpmath.exp(z[s]) / den
+    idx = []
+    for h in range(Hkv):
+        order = sorted(range(S), key=lambda s: (-shat[h][s], s))
+        idx.append(sorted(order[:k]))
+    return np.array(idx, np.int32), shat
+
+
+@pytest.mark.parametrize("B,x,rows", [(4, 1, [1]), (5, 1, [2]), (4, 2, [1, 2]), (4, 3, [0, 1, 2]),
+                                      (5, 3, [1, 2, 3]), (4, 4, [0, 1, 2, 3])])
+def test_select_xq_matches_50_digit_bruteforce_on_the_centred_rows(B, x, rows):
+    """x rows centred in the block (the lower middle row for even B, as the
+    centre [MASK] position of Eq. 2 ties there), each with its own softmax,
+    importance summed over rows and heads."""
+    rng = np.random.default_rng(40 + 10 * B + x)
+    q_sel = _rand(rng, (B, 4, 8), "bf16")
+    K = _rand(rng, (2, 23, 8), "bf16")
+    idx, shat = oracle.select_xq(q_sel, K, 6, x)
+    ref_idx, ref_shat = _mp_select_xq(q_sel, K, 6, rows)
+    np.testing.assert_array_equal(idx, ref_idx)
+    for h in range(2):
+        for s in range(23):
+            assert abs(shat[h, s] - float(ref_shat[h][s])) <= 1e-14 * float(ref_shat[h][s])
+
+
+def test_select_xq_one_row_is_the_mean_selection_of_that_row():
+    """x = 1 scores with the centre row alone: exactly what the mean
+    selection computes when every block row equals that row."""
+    rng = np.random.default_rng(21)
+    for B in (1, 4, 7, 32):
+        q_sel = _rand(rng, (B, 8, 32), "bf16")
+        K = _rand(rng, (2, 500, 32), "bf16")
+        c = (B - 1) // 2
+        same = np.repeat(q_sel[c:c + 1], B, axis=0)
+        idx1, s1 = oracle.select_xq(q_sel, K, 25, 1)
+        idx0, s0, _, _ = oracle.select(same, K, 25)
+        np.testing.assert_array_equal(idx1, idx0)
+        np.testing.assert_array_equal(s1, s0)
+
+
+@pytest.mark.parametrize("B,x", [(8, 2), (8, 5), (8, 8), (6, 3)])
+def test_select_xq_is_the_sum_of_single_row_importances(B, x):
+    rng = np.random.default_rng(B * 10 + x)
+    q_sel = _rand(rng, (B, 4, 16), "f32")
+    K = _rand(rng, (2, 300, 16), "f32")
+    _, sx = oracle.select_xq(q_sel, K, 10, x)
+    c0 = (B - x) // 2
+    want = np.zeros_like(sx)
+    for i in range(c0, c0 + x):
+        _, si, _, _ = oracle.select(np.repeat(q_sel[i:i + 1], B, axis=0), K, 10)
+        want += si
+    np.testing.assert_allclose(sx, want, rtol=1e-13)
+    np.testing.assert_allclose(sx.sum(1), x * 2, rtol=1e-13)   # x rows x G = 2 heads
+
+
+def test_select_xq_importance_reproduces_sdpa_outputs():
+    """sum_s s_hat[h,s] v_s is the sum of the attention outputs of the x
+    window rows over the heads of the group."""
+    rng = np.random.default_rng(77)
+    B, x, G, Hkv, d, S = 6, 4, 2, 2, 16, 60
+    q_sel = _rand(rng, (B, G * Hkv, d), "f64")
+    K = _rand(rng, (Hkv, S, d), "f64")
+    V = rng.standard_normal((Hkv, S, d))
+    _, shat = oracle.select_xq(q_sel, K, 5, x)
+    c0 = (B - x) // 2
+    q = torch.from_numpy(q_sel[c0:c0 + x]).permute(1, 0, 2)          # [Hq][x][d]
+    kt = torch.from_numpy(K).repeat_interleave(G, 0)
+    vt = torch.from_numpy(V).repeat_interleave(G, 0)
+    o = F.scaled_dot_product_attention(q, kt, vt)                    # [Hq][x][d]
+    want = o.sum(1).reshape(Hkv, G, d).sum(1).numpy()
+    got = np.einsum("hs,hsd->hd", shat, V)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
+def test_select_xq_ties_go_to_lower_index():
+    q = np.ones((3, 1, 8))
+    idx, _ = oracle.select_xq(q, np.zeros((1, 40, 8)), 7, 2)
+    np.testing.assert_array_equal(idx[0], np.arange(7))
+
+
 @pytest.mark.parametrize("pos", [0, 1, 63, 64, 127, 128, 500, 998, 999])
 def test_planted_key_anywhere_is_selected(pos):
     """Every prefix entry is scored: a dominant key is found at any position."""
