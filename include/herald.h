@@ -12,6 +12,11 @@
  *                      sec. IV-A.2), scores over every cached token, GQA
  *                      importance s_hat_h[s] = sum_g exp(s[g,s]-m_g)/l_g and
  *                      one top-k per KV head (sec. IV-B.4).
+ *   herald_select_xq   the same selection with x query rows of the block
+ *                      used as they are: x = 1 is the paper's centre [MASK]
+ *                      query (sec. IV-A.2, Eq. 2), x = B every block query;
+ *                      the cost grows with x (the query-count trade-off of
+ *                      sec. IV-A.2).
  *   herald_gather      copies the selected K/V rows into a sparse pool
  *                      (sec. IV-B.3).
  *   herald_block_attn  B-query GQA attention over a context (a pool, or a
@@ -140,6 +145,34 @@ herald_status herald_select(const herald_heads *heads, int32_t batch,
                             const herald_kv *kv, const int32_t *k_per_seq,
                             int32_t k_max, int32_t *idx_out, void *ws,
                             size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes needed by herald_select_xq for these sizes (0 if invalid,
+ * including x < 1 or x * H_q / H_kv > 512). Grows with x: the fp64 scores of
+ * x * H_q / H_kv score rows per cached row are kept. */
+size_t herald_select_xq_workspace(const herald_heads *heads, int32_t batch,
+                                  int32_t x, int64_t max_seq_len);
+
+/*
+ * Selection with x query rows (sec. IV-A.2). The rows are the x centred in
+ * the block, c0 = floor((block - x) / 2) to c0 + x - 1, each used as it is
+ * (no mean): x = 1 takes the centre [MASK] position, which Eq. 2 makes the
+ * representative (for even block sizes the two middle rows tie; the lower is
+ * taken); x = block takes every query of the block. Every (row, query head)
+ * pair is a score row with its own softmax statistics over the full cache,
+ * and the importance of a cached row for KV head h is the sum of its
+ * softmax-normalised scores over the x rows and the G = H_q / H_kv query
+ * heads of h (the G-sum of sec. IV-B.4 taken over query rows as well; the
+ * paper states no rule for x > 1, this is the library's reading).
+ *   x         host: 1 <= x <= block, x * G <= 512.
+ * Every other argument, the output, the fp64 ranking keys and the tie rule
+ * are as for herald_select; ws must hold herald_select_xq_workspace() bytes
+ * for this x and be 256-byte aligned.
+ */
+herald_status herald_select_xq(const herald_heads *heads, int32_t batch,
+                               int32_t block, int32_t x, const void *q_sel,
+                               const herald_kv *kv, const int32_t *k_per_seq,
+                               int32_t k_max, int32_t *idx_out, void *ws,
+                               size_t ws_bytes, hipStream_t stream);
 
 /*
  * Gather (sec. IV-B.3): for each (b, h) and j < k_b, copies row idx[b][h][j]

@@ -158,6 +158,38 @@ herald_status herald_select(const herald_heads *heads, int32_t batch, int32_t bl
                                   k_per_seq, k_max, idx_out, layout, stream));
 }
 
+size_t herald_select_xq_workspace(const herald_heads *heads, int32_t batch, int32_t x,
+                                  int64_t max_seq_len) {
+  if (check_heads(heads) != HERALD_OK || batch < 1 || max_seq_len < 1 || x < 1) return 0;
+  const int64_t V = (int64_t)x * (heads->num_q_heads / heads->num_kv_heads);
+  if (V > kMaxScoreRows) return 0;
+  // the selection workspace with V score rows per KV head in place of G
+  return select_ws_bytes(batch, (int)V * heads->num_kv_heads, heads->num_kv_heads,
+                         heads->head_dim, max_seq_len, nullptr, nullptr);
+}
+
+herald_status herald_select_xq(const herald_heads *heads, int32_t batch, int32_t block,
+                               int32_t x, const void *q_sel, const herald_kv *kv,
+                               const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
+                               void *ws, size_t ws_bytes, hipStream_t stream) {
+  herald_status st;
+  if ((st = check_heads(heads)) != HERALD_OK) return st;
+  if ((st = check_block(block)) != HERALD_OK) return st;
+  if (batch < 1 || x < 1 || x > block || !q_sel || !aligned16(q_sel) || !k_per_seq || !idx_out)
+    return HERALD_ERR_INVALID_ARG;
+  const int V = x * (heads->num_q_heads / heads->num_kv_heads);
+  if (V > kMaxScoreRows) return HERALD_ERR_UNSUPPORTED;
+  if ((st = check_kv(heads, kv, false)) != HERALD_OK) return st;
+  if (k_max < 1 || k_max > kv->max_seq_len) return HERALD_ERR_INVALID_ARG;
+  const size_t need = herald_select_xq_workspace(heads, batch, x, kv->max_seq_len);
+  if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
+  SelectWs layout;
+  select_ws_bytes(batch, V * heads->num_kv_heads, heads->num_kv_heads, heads->head_dim,
+                  kv->max_seq_len, &layout, reinterpret_cast<char *>(ws));
+  return hip_status(launch_select_xq(*heads, batch, block, x, q_sel, view_of(kv), k_per_seq,
+                                     k_max, idx_out, layout, stream));
+}
+
 herald_status herald_gather(const herald_heads *heads, int32_t batch, const herald_kv *kv,
                             const int32_t *idx, const int32_t *k_per_seq, int32_t k_max,
                             const herald_pool *dst, int32_t dst_row0, hipStream_t stream) {

@@ -86,7 +86,7 @@ __device__ __forceinline__ int clamp_k(int k, int64_t S, int k_max) {
 namespace herald {
 
 struct SelectWs {
-  double *qbar;     // [b][Hkv][d][G]
+  double *qbar;     // [b][Hkv][d][G]      (G: score rows per KV head)
   double *espill;   // [b][Hkv][S_pad][G]
   double *part;     // [b][Hkv][nchunk][G][2]
   uint64_t *keys;   // [b][Hkv][S_pad]
@@ -100,6 +100,17 @@ constexpr int kHistBins = 2048;       // first-level radix bins (key >> 52)
 
 size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
                        SelectWs *layout, char *base);
+
+// Largest number of score rows (query rows x query heads of a group) per KV
+// head that the x-row selection takes.
+constexpr int kMaxScoreRows = 512;
+
+// Selection with x query rows of the block (the workspace laid out for
+// V = x * G score rows per KV head in place of G).
+hipError_t launch_select_xq(const herald_heads &hd, int batch, int block, int x,
+                            const void *q_sel, const KvView &kv, const int32_t *k_per_seq,
+                            int k_max, int32_t *idx_out, const SelectWs &ws,
+                            hipStream_t stream);
 
 hipError_t launch_select(const herald_heads &hd, int batch, int block,
                          const void *q_sel, const KvView &kv, int64_t max_seq_len,

@@ -499,6 +499,245 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
     if (sh_hist[t]) atomicAdd(&hist[bh * kHistBins + t], sh_hist[t]);
 }
 
+// ---------------------------------------------------------------- x query rows
+// The x rows centred in the block, c0 = (block - x) / 2 ..., converted exactly
+// to fp64: qx[b][h][e][v] with score row v = i * G + g for window row c0 + i
+// and query head h * G + g. Clears the first-level histogram.
+template <bool BF16>
+__global__ __launch_bounds__(256) void rows_kernel(const void *__restrict__ q_sel,
+                                                   double *__restrict__ qx,
+                                                   uint32_t *__restrict__ hist, int block,
+                                                   int x, int Hq, int Hkv, int D) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int G = Hq / Hkv, V = x * G, c0 = (block - x) / 2;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  for (int t = blockIdx.z * 256 + threadIdx.x; t < D * V; t += gridDim.z * 256) {
+    const int e = t / V, v = t % V, i = v / G, g = v % G;
+    const int64_t src = (((int64_t)b * block + c0 + i) * Hq + h * G + g) * D + e;
+    const float f = BF16 ? bf16_lo(reinterpret_cast<const uint16_t *>(q_sel)[src])
+                         : reinterpret_cast<const float *>(q_sel)[src];
+    qx[(bh * D + e) * V + v] = (double)f;
+  }
+  if (blockIdx.z == 0)
+    for (int i = threadIdx.x; i < kHistBins; i += 256) hist[bh * kHistBins + i] = 0u;
+}
+
+// Scores of V > 4 score rows per KV head. The fp64 MFMA's operands swap roles
+// against score_mfma_kernel: A holds 16 score rows (4 per block, a different
+// 4 in each block) and B holds 4 cached rows, the same in every block, so one
+// v_mfma_f64_4x4x4_4b forms 4 cached rows x 16 score rows. Lane l of A holds
+// score row 4 ((l / 4) % 4) + l % 4 at element slot l / 16; lane l of B holds
+// cached row l % 4 at slot l / 16; the result of lane l is score row
+// 4 ((l / 4) % 4) + l / 16 of cached row l % 4. The head dimension is
+// enumerated in the same permuted order on both operands. A workgroup takes
+// one group of 16 score rows (zero past V) and one chunk of 2048 cached rows;
+// its 4 waves take interleaved 16-row tiles (4 chains of 4 rows) with the
+// next tile's loads in flight. The groups of one chunk have consecutive block
+// ids, so they read the chunk at about the same time. (With 512-byte rows a
+// tile is 2 chains of 4 rows, to keep two tiles in registers.)
+template <int D, bool BF16, bool PAGED>
+__global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
+                                                            const double *__restrict__ qx,
+                                                            double *__restrict__ zspill,
+                                                            double *__restrict__ part,
+                                                            int Hkv, int V, int nvg,
+                                                            int64_t S_pad, int nchunk,
+                                                            double scale) {
+  constexpr int ELT = BF16 ? 2 : 4;
+  constexpr int EPP = 16 / ELT;                 // elements per 16-byte piece
+  constexpr int NP = D * ELT / 64;              // pieces per lane and cached row
+  constexpr int NS = D / 4;                     // MFMA steps over the head dimension
+  constexpr int NW = 4;                         // waves per workgroup
+  constexpr int NCH = D * ELT > 256 ? 2 : 4;    // chains of 4 cached rows per tile
+  constexpr int TR = 4 * NCH;                   // cached rows per wave tile
+  constexpr int TPW = kScoreChunk / (TR * NW);  // tiles per wave
+  static_assert(NP * EPP == NS, "head dimension split");
+  __shared__ double red[NW][16], red2[NW][16];
+
+  const int vg = blockIdx.x % nvg, chunk = blockIdx.x / nvg, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = kv_len(kv, b);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S) return;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int kq = lane >> 4, blk = (lane >> 2) & 3, j = lane & 3;
+  const int va = vg * 16 + 4 * blk + j;    // A: score row of this lane
+  const int vz = vg * 16 + 4 * blk + kq;   // result: score row of this lane (cached row j)
+
+  // A operand of every step: the score row's query at the permuted element
+  double qa[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int e = (s / EPP) * (4 * EPP) + kq * EPP + s % EPP;
+    const double q = qx[(bh * D + e) * V + (va < V ? va : V - 1)];
+    qa[s] = va < V ? q : 0.0;
+  }
+
+  const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + kq * 16;
+  // 16-byte piece p of cached row s (the lane's slot): row-by-row page lookup
+  auto row_ptr = [&](int64_t s) -> const char * {
+    if (PAGED) {
+      const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s >> kv.page_shift)];
+      return kv.k + (page * kv.sp + (int64_t)h * kv.sh +
+                     (s & ((1 << kv.page_shift) - 1)) * kv.ss) * ELT + kq * 16;
+    }
+    return kbase + s * kv.ss * ELT;
+  };
+  auto tile_row0 = [&](int t) { return c0 + (int64_t)(t * NW + wave) * TR; };
+  // B operand pieces of a tile: chain c holds cached row r0 + 4c + j
+  uint4 kb[2][NCH][NP];
+  auto load_tile = [&](int t, uint4 (&dst)[NCH][NP]) {
+    const int64_t r0 = tile_row0(t);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int64_t s = r0 + 4 * c + j;
+      const bool ok = s < S;
+      const char *p = row_ptr(ok ? s : r0);
+#pragma unroll
+      for (int q = 0; q < NP; ++q) {
+        dst[c][q] = make_uint4(0u, 0u, 0u, 0u);
+        if (ok) dst[c][q] = ldg16_nt(p + q * 64);
+      }
+    }
+  };
+  auto elem = [&](const uint4 *pc, int s) -> double {
+    const uint4 v = pc[s / EPP];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    const int e = s % EPP;
+    if (BF16) return (double)((e & 1) ? bf16_hi(w[e >> 1]) : bf16_lo(w[e >> 1]));
+    return (double)__uint_as_float(w[e]);
+  };
+
+  double m_l = -INFINITY, l_l = 0.0;
+  auto step = [&](int t, uint4 (&cur)[NCH][NP], uint4 (&nxt)[NCH][NP]) -> bool {
+    const int64_t r0 = tile_row0(t);
+    if (r0 >= S) return false;  // uniform: later tiles of this wave start later still
+    if (t + 1 < TPW && tile_row0(t + 1) < S) load_tile(t + 1, nxt);
+    double acc[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) acc[c] = 0.0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f64_4x4x4f64(qa[s], elem(cur[c], s), acc[c], 0, 0, 0);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int64_t s = r0 + 4 * c + j;
+      if (vz < V && s < S) {
+        const double z = acc[c] * scale;
+        zspill[(bh * S_pad + s) * V + vz] = z;
+        const double dz = z - m_l;
+        const double e = exp(-fabs(dz));
+        const bool up = dz > 0.0;
+        l_l = up ? fma(l_l, e, 1.0) : l_l + e;
+        m_l = up ? z : m_l;
+      }
+    }
+    return true;
+  };
+  load_tile(0, kb[0]);
+#pragma unroll 1
+  for (int t = 0; t < TPW; t += 2) {
+    if (!step(t, kb[0], kb[1])) break;
+    if (!step(t + 1, kb[1], kb[0])) break;
+  }
+
+  // chunk statistics of each score row: over its 4 cached-row lanes, then the waves
+  double m = m_l;
+  m = fmax(m, __shfl_xor(m, 1, 64));
+  m = fmax(m, __shfl_xor(m, 2, 64));
+  const int slot = 4 * blk + kq;  // score row within the group
+  if (j == 0) red[wave][slot] = m;
+  __syncthreads();
+  const double mc = fmax(fmax(red[0][slot], red[1][slot]), fmax(red[2][slot], red[3][slot]));
+  double v = m_l == -INFINITY ? 0.0 : l_l * exp(m_l - mc);
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  if (j == 0) red2[wave][slot] = v;
+  __syncthreads();
+  if (wave == 0 && j == 0 && vz < V) {
+    double *p = part + ((bh * nchunk + chunk) * V + vz) * 2;
+    p[0] = mc;
+    p[1] = ((red2[0][slot] + red2[1][slot]) + red2[2][slot]) + red2[3][slot];
+  }
+}
+
+// GQA importance for any number V of score rows per KV head: as norm_kernel,
+// with the statistics in LDS and LPR lanes per cached row (a power of two,
+// up to 64) summing the V terms, combined by a butterfly of shuffles (every
+// lane of the row ends with the same sum, so equal score rows give equal keys).
+__global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restrict__ lens,
+                                                        const double *__restrict__ zspill,
+                                                        const double *__restrict__ part,
+                                                        uint64_t *__restrict__ keys,
+                                                        uint32_t *__restrict__ hist, int Hkv,
+                                                        int V, int64_t S_pad, int nchunk,
+                                                        int64_t max_len) {
+  __shared__ uint32_t sh_hist[kHistBins];
+  __shared__ double sm[kMaxScoreRows], sinv[kMaxScoreRows];
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S) return;
+  const int nch = (int)((S + kScoreChunk - 1) / kScoreChunk);
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int t = threadIdx.x; t < kHistBins; t += 256) sh_hist[t] = 0u;
+
+  // every workgroup of this (b, h) merges the same partials in the same order
+  for (int v = wave; v < V; v += 4) {
+    double m = -INFINITY, l = 0.0;
+    for (int c = lane; c < nch; c += 64) {
+      const double *p = part + ((bh * nchunk + c) * V + v) * 2;
+      merge_ml(m, l, p[0], p[1]);
+    }
+#pragma unroll
+    for (int off = 1; off <= 32; off <<= 1) {
+      const double m2 = __shfl_xor(m, off, 64);
+      const double l2 = __shfl_xor(l, off, 64);
+      if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
+      else merge_ml(m, l, m2, l2);
+    }
+    if (lane == 0) { sm[v] = m; sinv[v] = 1.0 / l; }
+  }
+  __syncthreads();
+
+  int lpr = 1;
+  while (lpr < V && lpr < 64) lpr <<= 1;
+  const int rpi = 64 / lpr;                 // cached rows per wave and round
+  const int sub = lane / lpr, q = lane % lpr;
+  const int64_t c1 = min(c0 + (int64_t)kScoreChunk, S);
+  for (int64_t base = c0 + (int64_t)wave * rpi; base < c1; base += 4 * rpi) {
+    const int64_t s = base + sub;
+    const bool valid = s < c1;
+    double acc = 0.0;
+    if (valid) {
+      const double *zz = zspill + (bh * S_pad + s) * V;
+      for (int v = q; v < V; v += lpr) acc += exp(zz[v] - sm[v]) * sinv[v];
+    }
+    for (int off = lpr >> 1; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    const bool lead = valid && q == 0;
+    uint64_t key = 0;
+    if (lead) {
+      key = (uint64_t)__double_as_longlong(acc);
+      keys[bh * S_pad + s] = key;
+    }
+    const uint32_t bin = (uint32_t)(key >> 52) & (kHistBins - 1);
+    uint64_t pending = __ballot(lead);
+    while (pending) {
+      const int leader = __ffsll((unsigned long long)pending) - 1;
+      const uint32_t lb = __shfl(bin, leader, 64);
+      const uint64_t same = __ballot(lead && bin == lb) & pending;
+      if (lane == leader) atomicAdd(&sh_hist[lb], (uint32_t)__popcll(same));
+      pending &= ~same;
+    }
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < kHistBins; t += 256)
+    if (sh_hist[t]) atomicAdd(&hist[bh * kHistBins + t], sh_hist[t]);
+}
+
 // ---------------------------------------------------------------- topk
 // Block-wide exclusive scan of one int per thread (1024 threads).
 __device__ __forceinline__ int block_excl_scan(int v, int *wsum, int *total) {
@@ -744,6 +983,52 @@ hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView
   return hipGetLastError();
 }
 
+
+template <int D, int V, bool BF16>
+void launch_score_norm_small(const KvView &kv, int batch, int Hkv, const SelectWs &ws,
+                             double scale, hipStream_t stream) {
+  const dim3 grid(ws.nchunk, Hkv, batch);
+  if (kv.pt)
+    score_mfma_kernel<D, V, BF16, true><<<grid, 256, 0, stream>>>(
+        kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+  else
+    score_mfma_kernel<D, V, BF16, false><<<grid, 256, 0, stream>>>(
+        kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+  norm_kernel<V><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv,
+                                           ws.S_pad, ws.nchunk, kv.max_len);
+}
+
+template <int D, bool BF16>
+hipError_t launch_select_xq_t(int batch, int block, int x, const void *q_sel,
+                              const KvView &kv, int Hq, int Hkv, const int32_t *k_per_seq,
+                              int k_max, int32_t *idx_out, const SelectWs &ws,
+                              hipStream_t stream) {
+  const int V = x * (Hq / Hkv);
+  const double scale = 1.0 / sqrt((double)D);
+  const int zb = min((D * V + 255) / 256, 64);
+  rows_kernel<BF16><<<dim3(Hkv, batch, zb), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist, block,
+                                                             x, Hq, Hkv, D);
+  if (V == 1) launch_score_norm_small<D, 1, BF16>(kv, batch, Hkv, ws, scale, stream);
+  else if (V == 2) launch_score_norm_small<D, 2, BF16>(kv, batch, Hkv, ws, scale, stream);
+  else if (V == 4) launch_score_norm_small<D, 4, BF16>(kv, batch, Hkv, ws, scale, stream);
+  else {
+    const int nvg = (V + 15) / 16;
+    const dim3 grid_s(ws.nchunk * nvg, Hkv, batch);
+    if (kv.pt)
+      score_rows_kernel<D, BF16, true><<<grid_s, 256, 0, stream>>>(
+          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, ws.nchunk, scale);
+    else
+      score_rows_kernel<D, BF16, false><<<grid_s, 256, 0, stream>>>(
+          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, ws.nchunk, scale);
+    norm_rows_kernel<<<dim3(ws.nchunk, Hkv, batch), 256, 0, stream>>>(
+        kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv, V, ws.S_pad, ws.nchunk,
+        kv.max_len);
+  }
+  topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
+      kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -770,6 +1055,25 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
     layout->nchunk = nchunk;
   }
   return off;
+}
+
+hipError_t launch_select_xq(const herald_heads &hd, int batch, int block, int x,
+                            const void *q_sel, const KvView &kv, const int32_t *k_per_seq,
+                            int k_max, int32_t *idx_out, const SelectWs &ws,
+                            hipStream_t stream) {
+  const bool bf = hd.dtype == HERALD_BF16;
+  const int Hq = hd.num_q_heads, Hkv = hd.num_kv_heads;
+  if (hd.head_dim == 64)
+    return bf ? launch_select_xq_t<64, true>(batch, block, x, q_sel, kv, Hq, Hkv, k_per_seq,
+                                             k_max, idx_out, ws, stream)
+              : launch_select_xq_t<64, false>(batch, block, x, q_sel, kv, Hq, Hkv, k_per_seq,
+                                              k_max, idx_out, ws, stream);
+  if (hd.head_dim == 128)
+    return bf ? launch_select_xq_t<128, true>(batch, block, x, q_sel, kv, Hq, Hkv, k_per_seq,
+                                              k_max, idx_out, ws, stream)
+              : launch_select_xq_t<128, false>(batch, block, x, q_sel, kv, Hq, Hkv,
+                                               k_per_seq, k_max, idx_out, ws, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_select(const herald_heads &hd, int batch, int block, const void *q_sel,

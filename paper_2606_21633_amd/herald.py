@@ -76,6 +76,11 @@ def lib():
     L.herald_select.restype = ctypes.c_int
     L.herald_select.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_p, ctypes.POINTER(KV),
                                 c_p, c_i32, c_p, c_p, c_sz, c_p]
+    L.herald_select_xq_workspace.restype = c_sz
+    L.herald_select_xq_workspace.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i64]
+    L.herald_select_xq.restype = ctypes.c_int
+    L.herald_select_xq.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i32, c_p,
+                                   ctypes.POINTER(KV), c_p, c_i32, c_p, c_p, c_sz, c_p]
     L.herald_gather.restype = ctypes.c_int
     L.herald_gather.argtypes = [ctypes.POINTER(Heads), c_i32, ctypes.POINTER(KV), c_p, c_p,
                                 c_i32, ctypes.POINTER(Pool), c_i32, c_p]
@@ -96,7 +101,8 @@ def lib():
 
 
 EXPORTS = ("herald_status_string", "herald_budget_tokens", "herald_select_workspace",
-           "herald_select", "herald_gather", "herald_block_attn_workspace",
+           "herald_select", "herald_select_xq_workspace", "herald_select_xq",
+           "herald_gather", "herald_block_attn_workspace",
            "herald_block_attn", "herald_decode_block_workspace", "herald_decode_block")
 
 
@@ -180,6 +186,19 @@ def select(hd: Heads, batch: int, block: int, q_sel, kv: KV, k_per_seq, k_max: i
                              _ptr(k_per_seq), k_max, _ptr(idx_out), _ptr(ws), nbytes,
                              _stream(stream))
     _check("herald_select", st)
+
+
+def select_xq_workspace(hd: Heads, batch: int, x: int, max_seq_len: int) -> int:
+    return int(lib().herald_select_xq_workspace(ctypes.byref(hd), batch, x, max_seq_len))
+
+
+def select_xq(hd: Heads, batch: int, block: int, x: int, q_sel, kv: KV, k_per_seq, k_max: int,
+              idx_out, ws, ws_bytes: int | None = None, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().herald_select_xq(ctypes.byref(hd), batch, block, x, _ptr(q_sel),
+                                ctypes.byref(kv), _ptr(k_per_seq), k_max, _ptr(idx_out),
+                                _ptr(ws), nbytes, _stream(stream))
+    _check("herald_select_xq", st)
 
 
 def gather(hd: Heads, batch: int, kv: KV, idx, k_per_seq, k_max: int, dst: Pool,

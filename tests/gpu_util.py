@@ -80,6 +80,17 @@ class Staged:
         torch.cuda.synchronize()
         return idx.cpu().numpy(), kps
 
+    def select_xq(self, x: int, kps_h: np.ndarray, k_max: int | None = None):
+        wl = self.wl
+        k_max = int(kps_h.max()) if k_max is None else k_max
+        kps = to_dev(kps_h.astype(np.int32))
+        idx = torch.full((wl.batch, wl.num_kv_heads, k_max), -7, dtype=torch.int32,
+                         device=DEV)
+        ws = H.workspace(H.select_xq_workspace(self.hd, wl.batch, x, self.S_max), DEV)
+        H.select_xq(self.hd, wl.batch, wl.block, x, self.q_sel, self.kv, kps, k_max, idx, ws)
+        torch.cuda.synchronize()
+        return idx.cpu().numpy()
+
 
 def assert_same_selection(got: np.ndarray, want: np.ndarray, s_hat: np.ndarray, k: int,
                           band: float = 1e-12) -> int:

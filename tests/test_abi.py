@@ -100,6 +100,44 @@ def test_select_validation():
                           stride_page=8 * 16 * 128)) == H.ERR_INVALID_ARG  # too few pages
 
 
+def _select_xq(hd=None, batch=2, block=4, x=2, q=FAKE, kv=None, kps=FAKE, k_max=52, idx=FAKE,
+               ws=FAKE * 256, ws_bytes=None):
+    hd = hd or H.heads(32, 8, 128, "bf16")
+    kv = kv or _kv()
+    if ws_bytes is None:
+        ws_bytes = H.select_xq_workspace(hd, batch, x, kv.max_seq_len) - 1  # one byte short
+    return H.lib().herald_select_xq(ctypes.byref(hd), batch, block, x, q, ctypes.byref(kv),
+                                    kps, k_max, idx, ws, ws_bytes, None)
+
+
+def test_select_xq_validation():
+    assert _select_xq() == H.ERR_WORKSPACE                    # one byte short
+    assert _select_xq(ws_bytes=H.select_workspace(H.heads(32, 8, 128, "bf16"), 2, 1024)) \
+        == H.ERR_WORKSPACE                                     # the x = 1 size is too small
+    assert _select_xq(x=0) == H.ERR_INVALID_ARG
+    assert _select_xq(x=5, ws_bytes=1 << 40) == H.ERR_INVALID_ARG   # x > block
+    assert _select_xq(q=None) == H.ERR_INVALID_ARG
+    assert _select_xq(q=FAKE + 2) == H.ERR_INVALID_ARG
+    assert _select_xq(kps=None) == H.ERR_INVALID_ARG
+    assert _select_xq(idx=None) == H.ERR_INVALID_ARG
+    assert _select_xq(block=65) == H.ERR_UNSUPPORTED
+    assert _select_xq(k_max=1025) == H.ERR_INVALID_ARG
+    assert _select_xq(kv=_kv(k=None)) == H.ERR_INVALID_ARG
+    assert _select_xq(hd=H.heads(32, 8, 96, "bf16")) == H.ERR_UNSUPPORTED
+
+
+def test_select_xq_workspace_grows_with_x():
+    hd = H.heads(32, 8, 128, "bf16")
+    w = [H.select_xq_workspace(hd, 16, x, 32768) for x in (1, 2, 4, 8, 16, 32)]
+    assert all(a < b for a, b in zip(w, w[1:]))
+    # the fp64 scores of x * G score rows per cached row dominate
+    assert w[-1] >= 16 * 8 * 32768 * 32 * 4 * 8
+    assert w[0] == H.select_workspace(hd, 16, 32768)
+    assert H.select_xq_workspace(hd, 16, 0, 32768) == 0
+    assert H.select_xq_workspace(H.heads(64, 8, 128, "bf16"), 1, 64, 100) > 0    # x G = 512
+    assert H.select_xq_workspace(H.heads(64, 8, 128, "bf16"), 1, 65, 100) == 0   # x G = 520
+
+
 def test_workspace_queries():
     hd = H.heads(32, 8, 128, "bf16")
     assert H.select_workspace(hd, 16, 32768) > 16 * 8 * 32768 * 8

@@ -122,6 +122,84 @@ def test_select_dominant_key_found_anywhere(pos):
     assert check_select(wl, inp, np.array([1]), 1) == 0
 
 
+# ---------------------------------------------------------------- x query rows
+
+
+def check_select_xq(wl, x, inp=None, kps_h=None, k_max=None, seqs=None):
+    inp = synth.make_host(wl) if inp is None else inp
+    st = Staged(wl, inp)
+    lens = inp["seq_lens"]
+    kps_h = budgets(lens, *wl.budget) if kps_h is None else np.asarray(kps_h, np.int32)
+    if k_max is None:
+        k_max = int(max(1, min(kps_h.max(), lens.max())))
+    got = st.select_xq(x, kps_h, k_max)
+    near = 0
+    for b in (range(wl.batch) if seqs is None else seqs):
+        S = int(lens[b])
+        k = int(min(max(kps_h[b], 0), S, k_max))
+        assert (got[b, :, k:] == -1).all()
+        if k == 0:
+            continue
+        kh, _ = seq_kv_host(inp, b)
+        idx_o, shat = oracle.select_xq(inp["q_sel"][b], kh, k, x)
+        for h in range(wl.num_kv_heads):
+            near += assert_same_selection(got[b, h, :k], idx_o[h], shat[h], k)
+    print(f"[select_xq] {wl.name} x={x}: near-ties={near}")
+    return near
+
+
+XQ = SMALL.replace(name="xq", block=32, seq_len=4500, seq_len_lo=900, seed=13)
+
+
+@pytest.mark.parametrize("x", [1, 2, 3, 4, 5, 8, 32])
+def test_select_xq_rows_g4(x):
+    # score rows x * 4: 4 (matrix-core scan with the rows as heads), 8, 12,
+    # 16, 20, 32, 128 (score-row scan, 1 to 8 groups of 16)
+    wl = XQ.replace(name=f"xq x{x}", num_q_heads=8, seed=50 + x)
+    assert check_select_xq(wl, x) == 0
+
+
+@pytest.mark.parametrize("G,d,dtype,x", [(1, 64, "bf16", 1), (1, 64, "bf16", 3), (2, 128, "bf16", 2),
+                                         (2, 64, "f32", 5), (4, 128, "f32", 4), (8, 64, "bf16", 7),
+                                         (1, 128, "bf16", 16)])
+def test_select_xq_group_and_dims(G, d, dtype, x):
+    wl = XQ.replace(name=f"xq G{G} d{d} {dtype} x{x}", num_q_heads=2 * G, dtype=dtype,
+                    head_dim=d, seed=60 + G + d + x)
+    assert check_select_xq(wl, x) == 0
+
+
+@pytest.mark.parametrize("x", [1, 6])
+def test_select_xq_paged_ragged(x):
+    wl = XQ.replace(name="xq paged", batch=5, page_size=16, seq_len=3000, seq_len_lo=17,
+                    num_q_heads=8, seed=31 + x)
+    assert check_select_xq(wl, x) == 0
+
+
+def test_select_xq_budget_edges_and_ties():
+    inp = synth.make_host(XQ.replace(num_q_heads=8))
+    wl = XQ.replace(num_q_heads=8)
+    assert check_select_xq(wl, 4, inp, np.array([1, 10 ** 6, 700]),
+                           int(inp["seq_lens"].max())) == 0
+    # every cached row identical: all importances equal, the lowest k indices
+    inp["k"][0, :, :] = inp["k"][0, :, 77:78]
+    st = Staged(wl, inp)
+    got = st.select_xq(8, np.array([300, 5, 5], np.int32), 300)
+    for h in range(wl.num_kv_heads):
+        np.testing.assert_array_equal(got[0, h], np.arange(300))
+
+
+def test_select_xq_one_row_differs_from_the_mean():
+    # the centre query and the mean of the block queries are different
+    # representatives: on random queries their selections differ
+    wl = XQ.replace(name="xq vs mean", batch=1, seq_len=4000, seq_len_lo=0, num_q_heads=8, seed=3)
+    inp = synth.make_host(wl)
+    st = Staged(wl, inp)
+    kps = budgets(inp["seq_lens"], *wl.budget)
+    a = st.select_xq(1, kps)
+    m, _ = st.select(kps)
+    assert (a != m).any()
+
+
 def test_select_layer_32k_workload_full():
     """All 16 sequences x 8 KV heads of the 8B-class 32K layer."""
     assert check_select(synth.LAYER_32K) == 0
