@@ -39,7 +39,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="layer32k",
-                    choices=["layer32k", "long128k", "tiny", "ragged", "pipeline36"])
+                    choices=["layer32k", "long128k", "tiny", "ragged", "pipeline36",
+                             "xq-sweep"])
     ap.add_argument("--blocks", type=int, default=3,
                     help="timed blocks of the 36-layer pipeline workload")
     ap.add_argument("--dense-layers", type=int, default=0,
@@ -78,6 +79,8 @@ def main():
         return bench_ragged(args)
     if args.workload == "pipeline36":
         return bench_pipeline36(args)
+    if args.workload == "xq-sweep":
+        return bench_xq_sweep(args)
     wl = {"layer32k": synth.LAYER_32K, "long128k": synth.LONG_128K,
           "tiny": synth.TINY_F32}[args.workload]
     b, B, T = wl.batch, wl.block, wl.steps
@@ -429,6 +432,68 @@ def bench_ragged(args):
                          "scan_GBps": round(kbytes / (ms_sel * 1e-3) / 1e9, 1),
                          "frac_hbm": round(kbytes / (ms_sel * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
            "gather": {"ms": round(ms_gat, 5)}, "device": torch.cuda.get_device_name(0)}
+    print(json.dumps(res), flush=True)
+
+
+def bench_xq_sweep(args):
+    """Selection cost against the number x of query rows (the query-count
+    trade-off of sec. IV-A.2), on the 8B-class layer: herald_select (mean of
+    the B queries) and herald_select_xq for x = 1 (centre query) ... 32 (every
+    block query). Each call scores all 16 x 8 x 32768 cached rows in fp64."""
+    import torch
+    from paper_2606_21633_amd import herald as H
+    from paper_2606_21633_amd import synth
+    dev = "cuda:0"
+    wl = synth.LAYER_32K
+    b, B = wl.batch, wl.block
+    Hq, Hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    G = Hq // Hkv
+    print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
+    inp = synth.make_host(wl)
+
+    def dv(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    S = int(inp["seq_lens"][0])
+    hd = H.heads(Hq, Hkv, d, wl.dtype)
+    k_b = H.budget_tokens(S, *wl.budget)
+    kk, vv, lens = dv(inp["k"]), dv(inp["v"]), dv(inp["seq_lens"])
+    kv = H.kv_view(kk, vv, lens, S)
+    q_sel = dv(inp["q_sel"])
+    kps = torch.full((b,), k_b, dtype=torch.int32, device=dev)
+    idx = torch.empty((b, Hkv, k_b), dtype=torch.int32, device=dev)
+    s = torch.cuda.current_stream()
+    kbytes = float(S) * d * 2 * b * Hkv
+    rows = []
+    ws = H.workspace(H.select_workspace(hd, b, S), dev)
+    ms = _timed(lambda: H.select(hd, b, B, q_sel, kv, kps, k_b, idx, ws), args.reps, s)
+    rows.append({"x": "mean", "ms": round(ms, 4), "scan_GBps": round(kbytes / ms / 1e6, 1)})
+    del ws
+    per_x = {}
+    for x in (1, 2, 4, 8, 16, 32):
+        ws = H.workspace(H.select_xq_workspace(hd, b, x, S), dev)
+        reps = max(3, args.reps // x)
+        ms = _timed(lambda: H.select_xq(hd, b, B, x, q_sel, kv, kps, k_b, idx, ws), reps, s)
+        flops = 2.0 * x * G * d * S * b * Hkv
+        per_x[x] = ms
+        rows.append({"x": x, "ms": round(ms, 4), "scan_GBps": round(kbytes / ms / 1e6, 1),
+                     "fp64_TFLOPs": round(flops / ms / 1e9, 2),
+                     "workspace_GB": round(ws.numel() / 1e9, 3)})
+        del ws
+        torch.cuda.empty_cache()
+    for r in rows:
+        if r["x"] != "mean":
+            r["speedup_vs_x32"] = round(per_x[32] / r["ms"], 2)
+    res = {"metric": "selection throughput vs query count x (x = 1 over x = 32)",
+           "value": round(per_x[32] / per_x[1], 3), "unit": "x", "n_gpus": 1,
+           "steps": args.reps, "warmup": 3, "ms_per_step": round(per_x[1], 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+           "data": "synthetic (seeded N(0,1) with planted heavy hitters and sinks)",
+           "config": {"workload": wl.name + " selection", "batch": b, "seq_len": S,
+                      "block": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                      "budget_tokens": k_b},
+           "sweep": rows, "device": torch.cuda.get_device_name(0)}
     print(json.dumps(res), flush=True)
 
 

@@ -200,6 +200,13 @@ def test_select_xq_one_row_differs_from_the_mean():
     assert (a != m).any()
 
 
+@pytest.mark.parametrize("x,seqs", [(1, [0, 15]), (8, [7]), (32, [3])])
+def test_select_xq_layer_32k_sampled(x, seqs):
+    """The 8B-class 32K layer as the x sweep runs it (all 16 sequences on the
+    GPU in one call), sampled sequences checked by the oracle."""
+    assert check_select_xq(synth.LAYER_32K, x, seqs=seqs) == 0
+
+
 def test_select_layer_32k_workload_full():
     """All 16 sequences x 8 KV heads of the 8B-class 32K layer."""
     assert check_select(synth.LAYER_32K) == 0
