@@ -22,6 +22,11 @@
 //            taking equal keys lowest index first.
 // Identical scores give bit-identical importances (one shift m_g per head for
 // every row), so exact ties are decided by index, as the definition says.
+//
+// Selection with x query rows (herald_select_xq) replaces repq by rows (the x
+// centred block rows converted to fp64) and, for more than 4 score rows
+// (query row, head) per KV head, score and norm by score_rows and norm_rows;
+// top-k is the same.
 #include <math.h>
 
 #include "common.h"
