@@ -24,6 +24,14 @@ Functions and the passages of the paper they follow:
                   sec. IV-B.4 extended over rows, a reading). x = 1 is the
                   centre [MASK] query of sec. IV-A.2 (Eq. 2; lower middle
                   row for even B); x = B every query of the block.
+* ``select_draft`` block n+1's selection with block n's draft KV appended
+                  for normalisation (sec. IV-B.2, steps 7-8): representative
+                  = mean (x = 0) or the x centred rows; the draft rows enter
+                  every softmax normaliser (m, l) but are never candidates
+                  (a reading: the completed block replaces them).
+* ``attn_groups`` the 2B-token step of sec. IV-B.2 (step 3): groups of B
+                  queries that attend to the same context, each to its own
+                  block KV and not to the other groups (custom masks).
 * ``gather``      copy of the selected rows into the sparse pool (sec. IV-B.3).
 * ``attn``        B-query GQA attention over a context plus the block's own
                   KV, unmasked (sec. II-A: bidirectional inside the block,
@@ -77,6 +85,9 @@ def _load():
     lib.herald_oracle_select_xq.restype = i32
     lib.herald_oracle_select_xq.argtypes = [i32, i32, i32, i32, i32, i64, p, i32, p, i32,
                                             i64, p, p]
+    lib.herald_oracle_select_draft.restype = i32
+    lib.herald_oracle_select_draft.argtypes = [i32, i32, i32, i32, i32, i64, p, i32, p, i32,
+                                               p, i32, i64, i64, p, p]
     lib.herald_oracle_gather.restype = i32
     lib.herald_oracle_gather.argtypes = [i32, i32, i64, p, i32, p, i64, i64, p]
     lib.herald_oracle_attn.restype = i32
@@ -162,6 +173,44 @@ def select_xq(q_sel, K, k: int, x: int):
     return idx, s_hat
 
 
+def select_draft(q_sel, K, tail, k: int, x: int = 0):
+    """One sequence. q_sel [B][Hq][d], K [Hkv][S][d], tail [n][Hkv][d] (or
+    None). Returns (idx int32 [Hkv][k] ascending, s_hat float64 [Hkv][S])."""
+    q, qt = _as_np(q_sel)
+    kk, kt = _as_np(K)
+    B, Hq, d = q.shape
+    Hkv, S, d2 = kk.shape
+    assert d == d2 and Hq % Hkv == 0
+    if tail is None:
+        tt, ttype, n = np.zeros((1, Hkv, d), np.float64), F64, 0
+    else:
+        tt, ttype = _as_np(tail)
+        assert tt.shape[1:] == (Hkv, d)
+        n = tt.shape[0]
+    idx = np.empty((Hkv, k), np.int32)
+    s_hat = np.empty((Hkv, S), np.float64)
+    rc = _load().herald_oracle_select_draft(B, int(x), Hq, Hkv, d, S, _ptr(q), qt, _ptr(kk),
+                                            kt, _ptr(tt), ttype, n, int(k), _ptr(s_hat),
+                                            _ptr(idx))
+    if rc != 0:
+        raise ValueError("herald_oracle_select_draft: bad arguments")
+    return idx, s_hat
+
+
+def attn_groups(q, ctx_k, ctx_v, blk_k, blk_v, groups: int):
+    """One sequence, `groups` groups of B queries. q [groups*B][Hq][d];
+    blk_k/blk_v [groups*B][Hkv][d]; group j's queries attend to the context
+    and to block rows j*B .. j*B+B-1 only. Returns float64 [groups*B][Hq][d]."""
+    qq, _ = _as_np(q)
+    bk, _ = _as_np(blk_k)
+    bv, _ = _as_np(blk_v)
+    n = qq.shape[0]
+    assert n % groups == 0 and bk.shape[0] == n and bv.shape[0] == n
+    B = n // groups
+    return np.concatenate([attn(qq[j * B:(j + 1) * B], ctx_k, ctx_v, bk[j * B:(j + 1) * B],
+                                bv[j * B:(j + 1) * B]) for j in range(groups)], axis=0)
+
+
 def gather(K, idx, cap: int | None = None):
     """pool[h][j] = K[h][idx[h][j]] (bit copy). K [Hkv][S][d], idx [Hkv][k]."""
     kk, kt = _as_np(K)
@@ -196,7 +245,7 @@ def attn(q, ctx_k, ctx_v, blk_k, blk_v):
     return out
 
 
-def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20):
+def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20, x: int = 0):
     """Sequential schedule of consecutive blocks of one sequence, one layer.
 
     K0, V0 [Hkv][S0][d]: the prefix cache before the first block.
@@ -206,6 +255,9 @@ def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20):
         k_steps, v_steps [T][B][Hkv][d]  the block's own KV per step,
         k_done, v_done [B][Hkv][d]  the completed block's KV,
         q_next [B][Hq][d]  block n+1's selection queries.
+    Optional per block: k_draft [B][Hkv][d], block n's draft KV, which block
+    n+1's selection appends for normalisation (sec. IV-B.2, steps 7-8);
+    x = 0 selects with the mean of q_next, x >= 1 with its x centred rows.
     Block n is denoised over pool(n); block n+1's selection runs over the
     prefix before block n; pool(n+1) = that top-k followed by block n's
     completed KV; then the cache grows by block n's completed KV.
@@ -223,7 +275,10 @@ def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20):
                               for t in range(T)]))
         S = Kc.shape[1]
         k = budget(S, num, den)
-        idx, _, _, _ = select(blk["q_next"], Kc, k)
+        if x == 0 and blk.get("k_draft") is None:
+            idx, _, _, _ = select(blk["q_next"], Kc, k)
+        else:
+            idx, _ = select_draft(blk["q_next"], Kc, blk.get("k_draft"), k, x)
         kd, _ = _as_np(blk["k_done"])
         vd, _ = _as_np(blk["v_done"])
         kd = np.ascontiguousarray(kd.transpose(1, 0, 2))

@@ -33,6 +33,16 @@
  *                          the block centre; for even B the two middle rows
  *                          tie and the lower is taken); x = B uses every
  *                          query of the block. Same top-k and tie rule.
+ *   herald_oracle_select_draft
+ *                          the selection of block n+1 with block n's draft KV
+ *                          appended for normalisation (sec. IV-B.2, steps 7
+ *                          and 8): the representative is the mean of the
+ *                          block's queries (x = 0) or the x centred rows; the
+ *                          draft rows' scores enter every score row's softmax
+ *                          statistics (m, l) but the draft rows are never
+ *                          candidates, since the completed block replaces
+ *                          them (a reading: the paper appends the draft to
+ *                          the pool it ranks).
  *   herald_oracle_gather   copy of the selected K/V rows into a dense pool
  *                          (sec. IV-B.3, the gather of the selected entries).
  *   herald_oracle_attn     B-query GQA attention of a block over a context
@@ -236,6 +246,91 @@ int herald_oracle_select_xq(int B, int x, int Hq, int Hkv, int d, int64_t S,
     }
     topk_ascending(r, S, k, idx_out + (int64_t)h * k);
     free(z); free(m); free(l); free(r);
+  }
+  return fail ? -1 : 0;
+}
+
+/*
+ * One sequence with a normalisation tail. q_sel [B][Hq][d]; K [Hkv][S][d];
+ * tail [n_tail][Hkv][d] (row t of head h at (t*Hkv + h)*d), n_tail >= 0.
+ * x = 0: one score row per query head, the mean of the B queries; x >= 1:
+ * the x centred rows as herald_oracle_select_xq. Writes s_hat [Hkv][S] (if
+ * non-NULL) and idx [Hkv][k] (ascending), candidates 0 .. S-1 only.
+ */
+int herald_oracle_select_draft(int B, int x, int Hq, int Hkv, int d, int64_t S,
+                               const void *q_sel, int q_type, const void *K,
+                               int k_type, const void *tail, int t_type,
+                               int64_t n_tail, int64_t k, double *s_hat_out,
+                               int32_t *idx_out) {
+  if (B < 1 || x < 0 || x > B || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 ||
+      S < 1 || k < 1 || k > S || n_tail < 0 || (n_tail > 0 && !tail))
+    return -1;
+  const int G = Hq / Hkv;
+  const int nrow = x == 0 ? 1 : x;   /* query rows per head */
+  const int c0 = (B - nrow) / 2;     /* first row of the centred window */
+  const int V = nrow * G;
+  const int64_t N = S + n_tail;      /* scored rows: prefix, then the tail */
+  const double scale = 1.0 / sqrt((double)d);
+  int fail = 0;
+
+#pragma omp parallel for schedule(dynamic) reduction(| : fail)
+  for (int h = 0; h < Hkv; ++h) {
+    double *qv = (double *)malloc(sizeof(double) * (size_t)V * d);
+    double *z = (double *)malloc(sizeof(double) * (size_t)V * N);
+    double *m = (double *)malloc(sizeof(double) * V);
+    double *l = (double *)malloc(sizeof(double) * V);
+    ranked *r = (ranked *)malloc(sizeof(ranked) * (size_t)S);
+    if (!qv || !z || !m || !l || !r) {
+      fail = 1;
+      free(qv); free(z); free(m); free(l); free(r);
+      continue;
+    }
+    /* the query of every score row v = i*G + g */
+    for (int i = 0; i < nrow; ++i)
+      for (int g = 0; g < G; ++g) {
+        const int v = i * G + g, hq = h * G + g;
+        for (int e = 0; e < d; ++e) {
+          if (x == 0) {
+            double acc = 0.0;
+            for (int j = 0; j < B; ++j)
+              acc += load_elem(q_sel, q_type, ((int64_t)j * Hq + hq) * d + e);
+            qv[v * d + e] = acc / (double)B;
+          } else {
+            qv[v * d + e] = load_elem(q_sel, q_type, ((int64_t)(c0 + i) * Hq + hq) * d + e);
+          }
+        }
+      }
+    /* scores over the prefix rows, then over the tail rows */
+    for (int v = 0; v < V; ++v)
+      for (int64_t s = 0; s < N; ++s) {
+        double acc = 0.0;
+        for (int e = 0; e < d; ++e) {
+          const double kv = s < S ? load_elem(K, k_type, ((int64_t)h * S + s) * d + e)
+                                  : load_elem(tail, t_type, ((s - S) * Hkv + h) * d + e);
+          acc += qv[v * d + e] * kv;
+        }
+        z[(int64_t)v * N + s] = acc * scale;
+      }
+    /* softmax statistics over prefix and tail */
+    for (int v = 0; v < V; ++v) {
+      double mx = -INFINITY;
+      for (int64_t s = 0; s < N; ++s)
+        if (z[(int64_t)v * N + s] > mx) mx = z[(int64_t)v * N + s];
+      double sum = 0.0;
+      for (int64_t s = 0; s < N; ++s) sum += exp(z[(int64_t)v * N + s] - mx);
+      m[v] = mx;
+      l[v] = sum;
+    }
+    /* importance of the prefix rows only: they are the candidates */
+    for (int64_t s = 0; s < S; ++s) {
+      double acc = 0.0;
+      for (int v = 0; v < V; ++v) acc += exp(z[(int64_t)v * N + s] - m[v]) / l[v];
+      r[s].key = acc;
+      r[s].idx = s;
+      if (s_hat_out) s_hat_out[(int64_t)h * S + s] = acc;
+    }
+    topk_ascending(r, S, k, idx_out + (int64_t)h * k);
+    free(qv); free(z); free(m); free(l); free(r);
   }
   return fail ? -1 : 0;
 }

@@ -449,3 +449,136 @@ def test_schedule_selects_from_prefix_before_current_block():
                  np.concatenate([pool_k, blocks[1]["k_steps"][0].transpose(1, 0, 2)], 1),
                  np.concatenate([pool_v, blocks[1]["v_steps"][0].transpose(1, 0, 2)], 1))
     np.testing.assert_allclose(outs[1][0], want, rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- draft lookahead
+
+
+@pytest.mark.parametrize("x", [0, 1, 3])
+def test_select_draft_without_tail_is_the_plain_selection(x):
+    rng = np.random.default_rng(60 + x)
+    q_sel = _rand(rng, (6, 8, 16), "bf16")
+    K = _rand(rng, (2, 400, 16), "bf16")
+    idx, s = oracle.select_draft(q_sel, K, None, 30, x)
+    if x == 0:
+        idx0, s0, _, _ = oracle.select(q_sel, K, 30)
+    else:
+        idx0, s0 = oracle.select_xq(q_sel, K, 30, x)
+    np.testing.assert_array_equal(idx, idx0)
+    np.testing.assert_array_equal(s, s0)
+
+
+@pytest.mark.parametrize("x", [0, 1, 2])
+def test_select_draft_tail_enters_the_normalisers_only(x):
+    """The draft rows are scored and normalised with the cache (the same
+    importance as a selection over cache + draft) but never selected: the
+    result is the top-k of the cache rows' importances alone."""
+    rng = np.random.default_rng(70 + x)
+    B, Hq, Hkv, d, S, n = 4, 8, 2, 16, 300, 4
+    q_sel = _rand(rng, (B, Hq, d), "f64")
+    K = _rand(rng, (Hkv, S, d), "f64")
+    tail = _rand(rng, (n, Hkv, d), "f64") * 3.0                 # strong draft keys
+    idx, s = oracle.select_draft(q_sel, K, tail, 25, x)
+    Kx = np.concatenate([K, tail.transpose(1, 0, 2)], axis=1)
+    if x == 0:
+        _, sx, _, _ = oracle.select(q_sel, Kx, 25)
+    else:
+        _, sx = oracle.select_xq(q_sel, Kx, 25, x)
+    np.testing.assert_array_equal(s, sx[:, :S])
+    for h in range(Hkv):
+        np.testing.assert_array_equal(idx[h], np.sort(np.argsort(-sx[h, :S], kind="stable")[:25]))
+    assert (s.sum(1) < (1 if x == 0 else x) * (Hq // Hkv) - 1e-3).all()   # draft mass excluded
+
+
+def test_select_draft_tail_shifts_the_ranking_between_heads():
+    """A draft row aligned with head 0's query dominates head 0's normaliser,
+    so the cache ranking follows head 1: the selection becomes head 1's
+    top-k of its scores."""
+    d, S = 8, 200
+    rng = np.random.default_rng(5)
+    q0 = np.zeros(d); q0[0] = 1.0
+    q1 = np.zeros(d); q1[1] = 1.0
+    q_sel = np.stack([q0, q1])[None] * 2.0                         # B = 1, Hq = 2, Hkv = 1
+    K = rng.standard_normal((1, S, d))
+    tail = np.zeros((1, 1, d)); tail[0, 0, 0] = 60.0               # exp(~42) swamps head 0
+    idx, _ = oracle.select_draft(q_sel, K, tail, 10)
+    by_h1 = np.sort(np.argsort(-K[0, :, 1], kind="stable")[:10])
+    np.testing.assert_array_equal(idx[0], by_h1)
+    idx0, _, _, _ = oracle.select(q_sel, K, 10)
+    assert not np.array_equal(idx0[0], by_h1)
+
+
+def test_attention_groups_are_masked_dense_attention():
+    """Two groups of B queries over one context: group j sees the context and
+    its own B block rows, not the other group's (block-diagonal mask)."""
+    rng = np.random.default_rng(88)
+    B, Hq, Hkv, d, n = 4, 4, 2, 16, 30
+    q = _rand(rng, (2 * B, Hq, d), "f64")
+    ck, cv = _rand(rng, (Hkv, n, d), "f64"), _rand(rng, (Hkv, n, d), "f64")
+    bk, bv = _rand(rng, (2 * B, Hkv, d), "f64"), _rand(rng, (2 * B, Hkv, d), "f64")
+    got = oracle.attn_groups(q, ck, cv, bk, bv, 2)
+    keys = np.concatenate([ck, bk.transpose(1, 0, 2)], axis=1)
+    vals = np.concatenate([cv, bv.transpose(1, 0, 2)], axis=1)
+    for j in range(2):
+        mask = np.zeros((Hkv, n + 2 * B), bool)
+        mask[:, :n] = True
+        mask[:, n + j * B:n + (j + 1) * B] = True
+        want = _sdpa(q[j * B:(j + 1) * B], keys, vals, mask)
+        np.testing.assert_allclose(got[j * B:(j + 1) * B], want, rtol=1e-12, atol=1e-13)
+    np.testing.assert_array_equal(oracle.attn_groups(q[:B], ck, cv, bk[:B], bv[:B], 1),
+                                  oracle.attn(q[:B], ck, cv, bk[:B], bv[:B]))
+
+
+@pytest.mark.parametrize("x", [0, 1])
+def test_full_budget_schedule_with_drafts_is_dense_decoding(x):
+    """At a 100% budget the draft changes no selection (everything is
+    selected): outputs equal those of the schedule without drafts."""
+    rng = np.random.default_rng(41)
+    B, T, Hq, Hkv, d, S0 = 4, 2, 4, 2, 16, 40
+    K0, V0 = _rand(rng, (Hkv, S0, d), "f64"), _rand(rng, (Hkv, S0, d), "f64")
+    blocks = []
+    for _ in range(3):
+        blocks.append(dict(
+            q_steps=_rand(rng, (T, B, Hq, d), "f64"),
+            k_steps=_rand(rng, (T, B, Hkv, d), "f64"),
+            v_steps=_rand(rng, (T, B, Hkv, d), "f64"),
+            k_done=_rand(rng, (B, Hkv, d), "f64"),
+            v_done=_rand(rng, (B, Hkv, d), "f64"),
+            k_draft=_rand(rng, (B, Hkv, d), "f64") * 4.0,
+            q_next=_rand(rng, (B, Hq, d), "f64")))
+    idx0 = np.tile(np.arange(S0, dtype=np.int32), (Hkv, 1))
+    with_d = oracle.decode_blocks(K0, V0, idx0, blocks, num=1, den=1, x=x)
+    without = oracle.decode_blocks(K0, V0, idx0, [{k: v for k, v in b.items() if k != "k_draft"}
+                                                  for b in blocks], num=1, den=1)
+    for a, b in zip(with_d, without):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_schedule_with_draft_selects_with_the_draft_as_tail():
+    """At 5% the draft KV of block n shapes block n+1's selection through the
+    normalisers: pool(n+1) = select_draft top-k of the prefix before block n,
+    then block n's completed KV."""
+    rng = np.random.default_rng(33)
+    B, T, Hq, Hkv, d, S0 = 2, 1, 4, 1, 8, 80
+    K0, V0 = _rand(rng, (Hkv, S0, d), "f64"), _rand(rng, (Hkv, S0, d), "f64")
+    mk = lambda: dict(q_steps=_rand(rng, (T, B, Hq, d), "f64"),
+                      k_steps=_rand(rng, (T, B, Hkv, d), "f64"),
+                      v_steps=_rand(rng, (T, B, Hkv, d), "f64"),
+                      k_done=_rand(rng, (B, Hkv, d), "f64"),
+                      v_done=_rand(rng, (B, Hkv, d), "f64"),
+                      k_draft=_rand(rng, (B, Hkv, d), "f64") * 5.0,
+                      q_next=_rand(rng, (B, Hq, d), "f64"))
+    blocks = [mk(), mk()]
+    idx0, _, _, _ = oracle.select(_rand(rng, (B, Hq, d), "f64"), K0, 4)
+    outs = oracle.decode_blocks(K0, V0, idx0, blocks, num=1, den=20, x=1)
+    k1 = oracle.budget(S0, 1, 20)
+    c = (B - 1) // 2
+    Kx = np.concatenate([K0, blocks[0]["k_draft"].transpose(1, 0, 2)], axis=1)
+    _, sx = oracle.select_xq(np.repeat(blocks[0]["q_next"][c:c + 1], B, axis=0), Kx, k1, 1)
+    sel = np.sort(np.argsort(-sx[0, :S0], kind="stable")[:k1])
+    pool_k = np.concatenate([K0[:, sel], blocks[0]["k_done"].transpose(1, 0, 2)], 1)
+    pool_v = np.concatenate([V0[:, sel], blocks[0]["v_done"].transpose(1, 0, 2)], 1)
+    want = _sdpa(blocks[1]["q_steps"][0],
+                 np.concatenate([pool_k, blocks[1]["k_steps"][0].transpose(1, 0, 2)], 1),
+                 np.concatenate([pool_v, blocks[1]["v_steps"][0].transpose(1, 0, 2)], 1))
+    np.testing.assert_allclose(outs[1][0], want, rtol=1e-12, atol=1e-13)
