@@ -17,11 +17,16 @@
  *                      query (sec. IV-A.2, Eq. 2), x = B every block query;
  *                      the cost grows with x (the query-count trade-off of
  *                      sec. IV-A.2).
+ *   herald_select_draft the next block's selection with the current
+ *                      block's draft KV appended for normalisation
+ *                      (draft-based lookahead, sec. IV-A.1, sec. IV-B.2).
  *   herald_gather      copies the selected K/V rows into a sparse pool
  *                      (sec. IV-B.3).
  *   herald_block_attn  B-query GQA attention over a context (a pool, or a
  *                      full cache for the dense baseline) plus the block's
- *                      own KV (sec. II-A, sec. V).
+ *                      own KV (sec. II-A, sec. V); herald_block_attn_groups
+ *                      runs several query groups that share the context
+ *                      (the 2B-token denoising + draft step, sec. IV-B.2).
  *   herald_decode_block one block over L layers as a two-stream pipeline:
  *                      the next block's selection on one stream, the T
  *                      denoising steps on the other, double-buffered pools
@@ -175,6 +180,29 @@ herald_status herald_select_xq(const herald_heads *heads, int32_t batch,
                                size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Selection of block n+1 with block n's draft KV appended (sec. IV-B.2,
+ * steps 7 and 8; sec. IV-A.1): the draft rows are scored with the cache and
+ * enter every score row's softmax statistics (m, l), so they shape the
+ * importance of the cached rows, but they are never candidates: the
+ * completed block replaces them (the library's reading; the paper appends
+ * the draft to the pool it ranks).
+ *   x         host: 0 ranks with the mean of the block's queries (as
+ *             herald_select), x >= 1 with its x centred rows (as
+ *             herald_select_xq; the paper's pipeline uses x = 1).
+ *   draft_k   device [batch][n_draft][H_kv][d] (the draft's K; V is not
+ *             read), 16-byte aligned; may be NULL if n_draft = 0.
+ *   n_draft   host, 0 <= n_draft <= 64 (n_draft = 0: no draft).
+ * Other arguments as herald_select; ws holds
+ * herald_select_xq_workspace(heads, batch, max(x, 1), kv->max_seq_len) bytes.
+ */
+herald_status herald_select_draft(const herald_heads *heads, int32_t batch,
+                                  int32_t block, int32_t x, const void *q_sel,
+                                  const herald_kv *kv, const void *draft_k,
+                                  int32_t n_draft, const int32_t *k_per_seq,
+                                  int32_t k_max, int32_t *idx_out, void *ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
+/*
  * Gather (sec. IV-B.3): for each (b, h) and j < k_b, copies row idx[b][h][j]
  * of kv's K and V into row dst_row0 + j of dst (bit-exact). Rows of dst
  * outside [dst_row0, dst_row0 + k_b) are not touched. idx is the output of
@@ -210,6 +238,27 @@ herald_status herald_block_attn(const herald_heads *heads, int32_t batch,
                                 const herald_kv *ctx, const void *blk_k,
                                 const void *blk_v, void *out, void *ws,
                                 size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Block attention of several query groups per sequence: the 2B-token step of
+ * sec. IV-B.2 (step 3), in which the denoising group and the draft group of
+ * block n attend to the same completed prefix but not to each other. Group j
+ * of sequence b is the block b * groups + j of a herald_block_attn call over
+ * batch * groups blocks whose context is ctx's sequence b:
+ *   q, out       device [batch][groups * block][H_q][d]
+ *   blk_k, blk_v device [batch][groups * block][H_kv][d]; group j's queries
+ *                see rows j * block .. j * block + block - 1 only.
+ *   ctx          as herald_block_attn, batch sequences (shared by groups).
+ *   groups       host, >= 1; groups = 1 is herald_block_attn.
+ * ws holds herald_block_attn_workspace(heads, batch * groups, block,
+ * ctx->max_seq_len) bytes.
+ */
+herald_status herald_block_attn_groups(const herald_heads *heads, int32_t batch,
+                                       int32_t block, int32_t groups,
+                                       const void *q, const herald_kv *ctx,
+                                       const void *blk_k, const void *blk_v,
+                                       void *out, void *ws, size_t ws_bytes,
+                                       hipStream_t stream);
 
 /* Tensors of one layer for herald_decode_block. */
 typedef struct {

@@ -138,24 +138,44 @@ size_t herald_select_workspace(const herald_heads *heads, int32_t batch, int64_t
                          max_seq_len, nullptr, nullptr);
 }
 
+// The selections share one path: x = 0 ranks with the mean of the block's
+// queries, x >= 1 with its x centred rows; tail rows (n_tail >= 0) enter the
+// softmax statistics only.
+static herald_status select_common(const herald_heads *heads, int32_t batch, int32_t block,
+                                   int32_t x, const void *q_sel, const herald_kv *kv,
+                                   const void *tail, int32_t n_tail, const int32_t *k_per_seq,
+                                   int32_t k_max, int32_t *idx_out, void *ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  herald_status st;
+  if ((st = check_heads(heads)) != HERALD_OK) return st;
+  if ((st = check_block(block)) != HERALD_OK) return st;
+  if (batch < 1 || x < 0 || x > block || !q_sel || !aligned16(q_sel) || !k_per_seq || !idx_out)
+    return HERALD_ERR_INVALID_ARG;
+  if (n_tail < 0 || n_tail > 64 || (n_tail > 0 && (!tail || !aligned16(tail))))
+    return HERALD_ERR_INVALID_ARG;
+  const int G = heads->num_q_heads / heads->num_kv_heads;
+  const int V = (x == 0 ? 1 : x) * G;
+  if (V > kMaxScoreRows) return HERALD_ERR_UNSUPPORTED;
+  if ((st = check_kv(heads, kv, false)) != HERALD_OK) return st;
+  if (k_max < 1 || k_max > kv->max_seq_len) return HERALD_ERR_INVALID_ARG;
+  const size_t need = herald_select_xq_workspace(heads, batch, x == 0 ? 1 : x, kv->max_seq_len);
+  if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
+  SelectWs layout;
+  select_ws_bytes(batch, V * heads->num_kv_heads, heads->num_kv_heads, heads->head_dim,
+                  kv->max_seq_len, &layout, reinterpret_cast<char *>(ws));
+  if (x == 0)
+    return hip_status(launch_select(*heads, batch, block, q_sel, view_of(kv), tail, n_tail,
+                                    k_per_seq, k_max, idx_out, layout, stream));
+  return hip_status(launch_select_xq(*heads, batch, block, x, q_sel, view_of(kv), tail, n_tail,
+                                     k_per_seq, k_max, idx_out, layout, stream));
+}
+
 herald_status herald_select(const herald_heads *heads, int32_t batch, int32_t block,
                             const void *q_sel, const herald_kv *kv,
                             const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
                             void *ws, size_t ws_bytes, hipStream_t stream) {
-  herald_status st;
-  if ((st = check_heads(heads)) != HERALD_OK) return st;
-  if ((st = check_block(block)) != HERALD_OK) return st;
-  if (batch < 1 || !q_sel || !aligned16(q_sel) || !k_per_seq || !idx_out)
-    return HERALD_ERR_INVALID_ARG;
-  if ((st = check_kv(heads, kv, false)) != HERALD_OK) return st;
-  if (k_max < 1 || k_max > kv->max_seq_len) return HERALD_ERR_INVALID_ARG;
-  const size_t need = herald_select_workspace(heads, batch, kv->max_seq_len);
-  if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
-  SelectWs layout;
-  select_ws_bytes(batch, heads->num_q_heads, heads->num_kv_heads, heads->head_dim,
-                  kv->max_seq_len, &layout, reinterpret_cast<char *>(ws));
-  return hip_status(launch_select(*heads, batch, block, q_sel, view_of(kv), kv->max_seq_len,
-                                  k_per_seq, k_max, idx_out, layout, stream));
+  return select_common(heads, batch, block, 0, q_sel, kv, nullptr, 0, k_per_seq, k_max,
+                       idx_out, ws, ws_bytes, stream);
 }
 
 size_t herald_select_xq_workspace(const herald_heads *heads, int32_t batch, int32_t x,
@@ -172,22 +192,18 @@ herald_status herald_select_xq(const herald_heads *heads, int32_t batch, int32_t
                                int32_t x, const void *q_sel, const herald_kv *kv,
                                const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
                                void *ws, size_t ws_bytes, hipStream_t stream) {
-  herald_status st;
-  if ((st = check_heads(heads)) != HERALD_OK) return st;
-  if ((st = check_block(block)) != HERALD_OK) return st;
-  if (batch < 1 || x < 1 || x > block || !q_sel || !aligned16(q_sel) || !k_per_seq || !idx_out)
-    return HERALD_ERR_INVALID_ARG;
-  const int V = x * (heads->num_q_heads / heads->num_kv_heads);
-  if (V > kMaxScoreRows) return HERALD_ERR_UNSUPPORTED;
-  if ((st = check_kv(heads, kv, false)) != HERALD_OK) return st;
-  if (k_max < 1 || k_max > kv->max_seq_len) return HERALD_ERR_INVALID_ARG;
-  const size_t need = herald_select_xq_workspace(heads, batch, x, kv->max_seq_len);
-  if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
-  SelectWs layout;
-  select_ws_bytes(batch, V * heads->num_kv_heads, heads->num_kv_heads, heads->head_dim,
-                  kv->max_seq_len, &layout, reinterpret_cast<char *>(ws));
-  return hip_status(launch_select_xq(*heads, batch, block, x, q_sel, view_of(kv), k_per_seq,
-                                     k_max, idx_out, layout, stream));
+  if (x < 1) return HERALD_ERR_INVALID_ARG;
+  return select_common(heads, batch, block, x, q_sel, kv, nullptr, 0, k_per_seq, k_max,
+                       idx_out, ws, ws_bytes, stream);
+}
+
+herald_status herald_select_draft(const herald_heads *heads, int32_t batch, int32_t block,
+                                  int32_t x, const void *q_sel, const herald_kv *kv,
+                                  const void *draft_k, int32_t n_draft,
+                                  const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
+                                  void *ws, size_t ws_bytes, hipStream_t stream) {
+  return select_common(heads, batch, block, x, q_sel, kv, draft_k, n_draft, k_per_seq, k_max,
+                       idx_out, ws, ws_bytes, stream);
 }
 
 herald_status herald_gather(const herald_heads *heads, int32_t batch, const herald_kv *kv,
@@ -218,11 +234,20 @@ herald_status herald_block_attn(const herald_heads *heads, int32_t batch, int32_
                                 const void *q, const herald_kv *ctx, const void *blk_k,
                                 const void *blk_v, void *out, void *ws, size_t ws_bytes,
                                 hipStream_t stream) {
+  return herald_block_attn_groups(heads, batch, block, 1, q, ctx, blk_k, blk_v, out, ws,
+                                  ws_bytes, stream);
+}
+
+herald_status herald_block_attn_groups(const herald_heads *heads, int32_t batch, int32_t block,
+                                       int32_t groups, const void *q, const herald_kv *ctx,
+                                       const void *blk_k, const void *blk_v, void *out,
+                                       void *ws, size_t ws_bytes, hipStream_t stream) {
   herald_status st;
   if ((st = check_heads(heads)) != HERALD_OK) return st;
   if ((st = check_block(block)) != HERALD_OK) return st;
-  if (batch < 1 || !q || !blk_k || !blk_v || !out || !aligned16(q) || !aligned16(blk_k) ||
-      !aligned16(blk_v) || !aligned16(out))
+  if (batch < 1 || groups < 1 || (int64_t)batch * groups > INT32_MAX / 1024 || !q || !blk_k ||
+      !blk_v || !out || !aligned16(q) || !aligned16(blk_k) || !aligned16(blk_v) ||
+      !aligned16(out))
     return HERALD_ERR_INVALID_ARG;
   if (!ctx || !ctx->seq_lens || ctx->max_seq_len < 0 || ctx->max_seq_len > INT32_MAX)
     return HERALD_ERR_INVALID_ARG;
@@ -230,11 +255,12 @@ herald_status herald_block_attn(const herald_heads *heads, int32_t batch, int32_
     herald_kv c = *ctx;
     if ((st = check_kv(heads, &c, true)) != HERALD_OK) return st;
   }
-  const size_t need = herald_block_attn_workspace(heads, batch, block, ctx->max_seq_len);
-  const AttnPlan p = attn_plan(*heads, batch, block, ctx->max_seq_len);
+  const size_t need = herald_block_attn_workspace(heads, batch * groups, block,
+                                                  ctx->max_seq_len);
+  const AttnPlan p = attn_plan(*heads, batch * groups, block, ctx->max_seq_len);
   if (p.nsplit > 1 && (!ws || !aligned256(ws) || ws_bytes < need)) return HERALD_ERR_WORKSPACE;
-  return hip_status(launch_block_attn(*heads, batch, block, q, view_of(ctx), ctx->max_seq_len,
-                                      blk_k, blk_v, out, ws, stream));
+  return hip_status(launch_block_attn(*heads, batch, block, groups, q, view_of(ctx),
+                                      ctx->max_seq_len, blk_k, blk_v, out, ws, stream));
 }
 
 size_t herald_decode_block_workspace(const herald_heads *heads, int32_t batch, int32_t block,
@@ -318,7 +344,7 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
       if (layer_dense(l)) continue;
       const herald_layer &L = layers[l];
       herald_kv cache = kv_of_pool(&L.cache, seq_lens, max_seq_len);
-      e = launch_select(*heads, batch, block, L.q_next, view_of(&cache), max_seq_len, k_next,
+      e = launch_select(*heads, batch, block, L.q_next, view_of(&cache), nullptr, 0, k_next,
                         k_max, idx, sel, s_retr);
       if (e == hipSuccess)
         e = launch_gather(*heads, batch, view_of(&cache), idx, k_next, k_max, pool_of(&L.idle),
@@ -336,7 +362,7 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
       const char *bk = reinterpret_cast<const char *>(L.blk_k) + t * kv_step * elt;
       const char *bv = reinterpret_cast<const char *>(L.blk_v) + t * kv_step * elt;
       char *o = reinterpret_cast<char *>(L.out) + t * L.out_step_stride * elt;
-      e = launch_block_attn(*heads, batch, block, q, view_of(&ctx), ctx.max_seq_len, bk, bv, o,
+      e = launch_block_attn(*heads, batch, block, 1, q, view_of(&ctx), ctx.max_seq_len, bk, bv, o,
                             attn_ws, s_main);
     }
   }

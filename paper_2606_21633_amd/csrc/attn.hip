@@ -32,13 +32,13 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Byte offset of row `key` of (b, h) among context rows then block rows.
-// Callers clamp key into [0, n_ctx + block).
+// Byte offset of row `key` of (b, h) among context rows (of context sequence
+// bc) then block rows. Callers clamp key into [0, n_ctx + block).
 __device__ __forceinline__ const char *row_ptr(const KvView &ctx, const char *ctxbase,
-                                               const char *blk, int b, int h, int64_t key,
-                                               int64_t n_ctx, int block, int Hkv, int D,
-                                               int elt) {
-  if (key < n_ctx) return ctxbase + kv_row(ctx, b, h, key) * elt;
+                                               const char *blk, int bc, int b, int h,
+                                               int64_t key, int64_t n_ctx, int block, int Hkv,
+                                               int D, int elt) {
+  if (key < n_ctx) return ctxbase + kv_row(ctx, bc, h, key) * elt;
   return blk + ((((int64_t)b * block + (key - n_ctx)) * Hkv + h) * D) * elt;
 }
 
@@ -104,7 +104,7 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
     const uint16_t *__restrict__ q, KvView ctx, const uint16_t *__restrict__ blk_k,
     const uint16_t *__restrict__ blk_v, uint16_t *__restrict__ out,
     float *__restrict__ part_o, float2 *__restrict__ part_ml, int block, int Hq, int Hkv,
-    int G, int M, int n_mblk, int nsplit, int keys_per_split, float sl2) {
+    int G, int M, int n_mblk, int nsplit, int keys_per_split, float sl2, int groups) {
   constexpr int KT = 32;             // keys per tile
   constexpr int CB = RW / 16;        // column blocks (16 query rows) per wave
   constexpr int NKS = D / 32;        // k-steps of K Q^T
@@ -141,10 +141,13 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
   }
   const int split = grp % nsplit;
   const int h = (grp / nsplit) % Hkv, b = grp / nsplit / Hkv;
+  // b indexes the query groups (queries, block KV, outputs); groups of one
+  // sequence share its context
+  const int bc = b / groups;
   const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int pipe = wv / NWP, w = wv % NWP;
   const int tid = threadIdx.x % NTH, lane = threadIdx.x & 63, q4 = lane >> 4, l16 = lane & 15;
-  const int64_t n_ctx = kv_len(ctx, b);
+  const int64_t n_ctx = kv_len(ctx, bc);
   const int64_t n_keys = n_ctx + block;
   const int64_t k_begin = (int64_t)split * keys_per_split;
   const int64_t k_end = min(k_begin + (int64_t)keys_per_split, n_keys);
@@ -181,8 +184,8 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
   // with x = tid + u * NTH, for K and V alike
   const int64_t crs = ctx.ss * 2;             // context row stride (bytes)
   const int64_t brs = (int64_t)Hkv * D * 2;   // block row stride (bytes)
-  const char *ckb = ctx.k + ((int64_t)b * ctx.sb + (int64_t)h * ctx.sh) * 2;
-  const char *cvb = ctx.v + ((int64_t)b * ctx.sb + (int64_t)h * ctx.sh) * 2;
+  const char *ckb = ctx.k + ((int64_t)bc * ctx.sb + (int64_t)h * ctx.sh) * 2;
+  const char *cvb = ctx.v + ((int64_t)bc * ctx.sb + (int64_t)h * ctx.sh) * 2;
   const char *bkb = reinterpret_cast<const char *>(blk_k) + ((int64_t)b * block * Hkv + h) * D * 2;
   const char *bvb = reinterpret_cast<const char *>(blk_v) + ((int64_t)b * block * Hkv + h) * D * 2;
   // Tile `it` of this pipeline (tile index it * P + pipe): K and V bases, row
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
 #pragma unroll
       for (int u = 0; u < LPT; ++u) {
         const int x = tid + u * NTH;
-        const int64_t e = kv_row(ctx, b, h, d.r0 + min(x / CPR, last)) * 2 + (x % CPR) * 16;
+        const int64_t e = kv_row(ctx, bc, h, d.r0 + min(x / CPR, last)) * 2 + (x % CPR) * 16;
         kx[u] = ldg16(ctx.k + e);
         vx[u] = ldg16(ctx.v + e);
       }
@@ -510,7 +513,7 @@ template <int D>
 __global__ __launch_bounds__(256) void attn_f32_kernel(
     const float *__restrict__ q, KvView ctx, const float *__restrict__ blk_k,
     const float *__restrict__ blk_v, float *__restrict__ out, int block, int Hq, int Hkv,
-    int G, int M, float scale) {
+    int G, int M, float scale, int groups) {
   constexpr int ND = (D + 63) / 64;
   const int h = blockIdx.y, b = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -518,7 +521,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   if (r >= M) return;
   const int g = r / block, i = r % block;
   const int64_t qoff = (((int64_t)b * block + i) * Hq + h * G + g) * D;
-  const int64_t n_ctx = kv_len(ctx, b);
+  const int bc = b / groups;  // context sequence of this query group
+  const int64_t n_ctx = kv_len(ctx, bc);
   const int64_t n_keys = n_ctx + block;
   const char *ck = ctx.k, *cv = ctx.v;
   const char *bk = reinterpret_cast<const char *>(blk_k);
@@ -531,7 +535,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     float logit = -INFINITY;
     if (key < n_keys) {
       const float *kr = reinterpret_cast<const float *>(
-          row_ptr(ctx, ck, bk, b, h, key, n_ctx, block, Hkv, D, 4));
+          row_ptr(ctx, ck, bk, bc, b, h, key, n_ctx, block, Hkv, D, 4));
       float acc = 0.f;
       for (int e = 0; e < D; ++e) acc = fmaf(q[qoff + e], kr[e], acc);
       logit = acc * scale;
@@ -551,7 +555,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     for (int jj = 0; jj < nvalid; ++jj) {
       const float pj = __shfl(p, jj, 64);
       const float *vr = reinterpret_cast<const float *>(
-          row_ptr(ctx, cv, bv, b, h, j0 + jj, n_ctx, block, Hkv, D, 4));
+          row_ptr(ctx, cv, bv, bc, b, h, j0 + jj, n_ctx, block, Hkv, D, 4));
 #pragma unroll
       for (int u = 0; u < ND; ++u) {
         const int d = lane + 64 * u;
@@ -623,9 +627,12 @@ AttnPlan attn_plan(const herald_heads &hd, int batch, int block, int64_t max_ctx
   return p;
 }
 
-hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, const void *q,
-                             const KvView &ctx, int64_t max_ctx, const void *blk_k,
-                             const void *blk_v, void *out, void *ws, hipStream_t stream) {
+hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, int groups,
+                             const void *q, const KvView &ctx, int64_t max_ctx,
+                             const void *blk_k, const void *blk_v, void *out, void *ws,
+                             hipStream_t stream) {
+  // the query groups of all sequences form one batch of batch * groups
+  batch *= groups;
   const AttnPlan p = attn_plan(hd, batch, block, max_ctx);
   const int G = hd.num_q_heads / hd.num_kv_heads;
   const int Hq = hd.num_q_heads, Hkv = hd.num_kv_heads, D = hd.head_dim;
@@ -635,11 +642,11 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, const
     if (D == 64)
       attn_f32_kernel<64><<<grid, 256, 0, stream>>>(
           (const float *)q, ctx, (const float *)blk_k, (const float *)blk_v, (float *)out,
-          block, Hq, Hkv, G, p.M, scale);
+          block, Hq, Hkv, G, p.M, scale, groups);
     else if (D == 128)
       attn_f32_kernel<128><<<grid, 256, 0, stream>>>(
           (const float *)q, ctx, (const float *)blk_k, (const float *)blk_v, (float *)out,
-          block, Hq, Hkv, G, p.M, scale);
+          block, Hq, Hkv, G, p.M, scale, groups);
     else
       return hipErrorInvalidValue;
     return hipGetLastError();
@@ -663,7 +670,7 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, const
     if (attr_err != hipSuccess) return attr_err;                                         \
     kfn<<<grid, NW_ * 4 * 64, kSmem, stream>>>(qq, ctx, bk, bv, oo, part_o, part_ml,      \
                                                block, Hq, Hkv, G, p.M, p.n_mblk,         \
-                                               p.nsplit, p.keys_per_split, sl2);         \
+                                               p.nsplit, p.keys_per_split, sl2, groups); \
   } else
   HERALD_ATTN(64, 32, 2, false) HERALD_ATTN(64, 32, 1, false) HERALD_ATTN(64, 16, 1, false)
   HERALD_ATTN(128, 32, 2, false) HERALD_ATTN(128, 32, 1, false) HERALD_ATTN(128, 16, 1, false)

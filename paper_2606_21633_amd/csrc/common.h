@@ -88,7 +88,8 @@ namespace herald {
 struct SelectWs {
   double *qbar;     // [b][Hkv][d][G]      (G: score rows per KV head)
   double *espill;   // [b][Hkv][S_pad][G]
-  double *part;     // [b][Hkv][nchunk][G][2]
+  double *part;     // [b][Hkv][nchunk + 1][G][2]: (max, sum exp) per chunk, then
+                    // of the normalisation tail
   uint64_t *keys;   // [b][Hkv][S_pad]
   uint32_t *hist;   // [b][Hkv][2048]
   int64_t S_pad;
@@ -106,14 +107,18 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
 constexpr int kMaxScoreRows = 512;
 
 // Selection with x query rows of the block (the workspace laid out for
-// V = x * G score rows per KV head in place of G).
+// V = x * G score rows per KV head in place of G). tail: [b][n_tail][Hkv][d]
+// rows that enter every score row's (max, sum exp) but are never ranked
+// (n_tail = 0: none).
 hipError_t launch_select_xq(const herald_heads &hd, int batch, int block, int x,
-                            const void *q_sel, const KvView &kv, const int32_t *k_per_seq,
-                            int k_max, int32_t *idx_out, const SelectWs &ws,
-                            hipStream_t stream);
+                            const void *q_sel, const KvView &kv, const void *tail, int n_tail,
+                            const int32_t *k_per_seq, int k_max, int32_t *idx_out,
+                            const SelectWs &ws, hipStream_t stream);
 
+// Selection with the mean of the block's queries as the representative;
+// tail as above.
 hipError_t launch_select(const herald_heads &hd, int batch, int block,
-                         const void *q_sel, const KvView &kv, int64_t max_seq_len,
+                         const void *q_sel, const KvView &kv, const void *tail, int n_tail,
                          const int32_t *k_per_seq, int k_max, int32_t *idx_out,
                          const SelectWs &ws, hipStream_t stream);
 
@@ -137,7 +142,10 @@ struct AttnPlan {
 
 AttnPlan attn_plan(const herald_heads &hd, int batch, int block, int64_t max_ctx);
 
-hipError_t launch_block_attn(const herald_heads &hd, int batch, int block,
+// groups query groups of `block` rows per sequence (q, blk_k/blk_v and out
+// hold batch * groups groups); the groups of sequence b share its context and
+// each sees only its own block KV.
+hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, int groups,
                              const void *q, const KvView &ctx, int64_t max_ctx,
                              const void *blk_k, const void *blk_v, void *out,
                              void *ws, hipStream_t stream);

@@ -52,6 +52,7 @@ template <int D, int G, bool BF16>
 __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_sel,
                                                    double *__restrict__ qbar,
                                                    uint32_t *__restrict__ hist,
+                                                   double *__restrict__ part, int nslot,
                                                    int block, int Hq, int Hkv) {
   constexpr int U = 64;  // loads in flight per thread: every block row at once
   const int h = blockIdx.x, b = blockIdx.y;
@@ -84,8 +85,15 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
     }
     qbar[(bh * D + e) * G + g] = acc / (double)block;
   }
-  if (blockIdx.z == 0)
+  if (blockIdx.z == 0) {
     for (int i = threadIdx.x; i < kHistBins; i += 256) hist[bh * kHistBins + i] = 0u;
+    // no normalisation tail unless tail_kernel fills its slot
+    if (threadIdx.x < G) {
+      double *p = part + ((bh * nslot + nslot - 1) * G + threadIdx.x) * 2;
+      p[0] = -INFINITY;
+      p[1] = 0.0;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- score (FMA)
@@ -101,7 +109,7 @@ __global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
                                                        double *__restrict__ zspill,
                                                        double *__restrict__ part,
                                                        int Hkv, int64_t S_pad,
-                                                       int nchunk, double scale) {
+                                                       int nslot, double scale) {
   constexpr int ELT = BF16 ? 2 : 4;
   constexpr int RB = D * ELT;         // bytes per cached row
   constexpr int LPR = RB / 16;        // lanes per row in one 1 KiB load
@@ -255,7 +263,7 @@ __global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
   __syncthreads();
   if (wave < 2 && lane < GH && (G > 1 || wave == 0)) {
     const int gg = lane, g = g0 + gg;
-    double *p = part + ((bh * nchunk + chunk) * G + g) * 2;
+    double *p = part + ((bh * nslot + chunk) * G + g) * 2;
     p[0] = fmax(red[half][gg], red[half + 2][gg]);
     p[1] = red2[half][gg] + red2[half + 2][gg];
   }
@@ -286,7 +294,7 @@ __global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
                                                             double *__restrict__ zspill,
                                                             double *__restrict__ part,
                                                             int Hkv, int64_t S_pad,
-                                                            int nchunk, double scale) {
+                                                            int nslot, double scale) {
   static_assert(G <= 4, "one MFMA column per query head of the group");
   constexpr int ELT = BF16 ? 2 : 4;
   constexpr int RB = D * ELT;                   // bytes per cached row
@@ -427,7 +435,7 @@ __global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
   if (lane < 4) red2[wave][lane] = v;
   __syncthreads();
   if (wave == 0 && lane < G) {
-    double *p = part + ((bh * nchunk + chunk) * G + lane) * 2;
+    double *p = part + ((bh * nslot + chunk) * G + lane) * 2;
     p[0] = mc;
     p[1] = ((red2[0][lane] + red2[1][lane]) + red2[2][lane]) + red2[3][lane];
   }
@@ -440,7 +448,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
                                                    const double *__restrict__ part,
                                                    uint64_t *__restrict__ keys,
                                                    uint32_t *__restrict__ hist, int Hkv,
-                                                   int64_t S_pad, int nchunk, int64_t max_len) {
+                                                   int64_t S_pad, int nslot, int64_t max_len) {
   __shared__ uint32_t sh_hist[kHistBins];
   __shared__ double sm[G], sinv[G];
   const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -456,8 +464,9 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
   // order, so all of them see bit-identical (m_g, l_g).
   for (int g = wave; g < G; g += 4) {
     double m = -INFINITY, l = 0.0;
-    for (int c = lane; c < nch; c += 64) {
-      const double *p = part + ((bh * nchunk + c) * G + g) * 2;
+    for (int c = lane; c <= nch; c += 64) {
+      const int slot = c < nch ? c : nslot - 1;  // the chunks, then the tail
+      const double *p = part + ((bh * nslot + slot) * G + g) * 2;
       merge_ml(m, l, p[0], p[1]);
     }
 #pragma unroll
@@ -511,8 +520,9 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
 template <bool BF16>
 __global__ __launch_bounds__(256) void rows_kernel(const void *__restrict__ q_sel,
                                                    double *__restrict__ qx,
-                                                   uint32_t *__restrict__ hist, int block,
-                                                   int x, int Hq, int Hkv, int D) {
+                                                   uint32_t *__restrict__ hist,
+                                                   double *__restrict__ part, int nslot,
+                                                   int block, int x, int Hq, int Hkv, int D) {
   const int h = blockIdx.x, b = blockIdx.y;
   const int G = Hq / Hkv, V = x * G, c0 = (block - x) / 2;
   const int64_t bh = (int64_t)b * Hkv + h;
@@ -523,8 +533,53 @@ __global__ __launch_bounds__(256) void rows_kernel(const void *__restrict__ q_se
                          : reinterpret_cast<const float *>(q_sel)[src];
     qx[(bh * D + e) * V + v] = (double)f;
   }
-  if (blockIdx.z == 0)
+  if (blockIdx.z == 0) {
     for (int i = threadIdx.x; i < kHistBins; i += 256) hist[bh * kHistBins + i] = 0u;
+    for (int v = threadIdx.x; v < V; v += 256) {  // no tail unless tail_kernel runs
+      double *p = part + ((bh * nslot + nslot - 1) * V + v) * 2;
+      p[0] = -INFINITY;
+      p[1] = 0.0;
+    }
+  }
+}
+
+// Softmax statistics of a normalisation tail: block n's draft KV, which
+// block n+1's selection appends (sec. IV-B.2, steps 7-8). For every score row
+// v, (max, sum of exp) of its scores over the n_tail tail rows (one lane
+// each, n_tail <= 64) go to the last partial slot, which norm merges after the
+// chunks; the tail rows are never ranked. tail: [b][n_tail][Hkv][D].
+template <bool BF16>
+__global__ __launch_bounds__(256) void tail_kernel(const double *__restrict__ qbar,
+                                                   const void *__restrict__ tail, int n_tail,
+                                                   double *__restrict__ part, int nslot,
+                                                   int Hkv, int V, int D, double scale) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int v = wave; v < V; v += 4) {
+    double z = -INFINITY;
+    if (lane < n_tail) {
+      const int64_t row = (((int64_t)b * n_tail + lane) * Hkv + h) * D;
+      double acc = 0.0;
+      for (int e = 0; e < D; ++e) {
+        const double kx = BF16 ? (double)bf16_lo(reinterpret_cast<const uint16_t *>(tail)[row + e])
+                               : (double)reinterpret_cast<const float *>(tail)[row + e];
+        acc = fma(qbar[(bh * D + e) * V + v], kx, acc);
+      }
+      z = acc * scale;
+    }
+    double m = z;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
+    double l = lane < n_tail ? exp(z - m) : 0.0;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) l += __shfl_xor(l, off, 64);
+    if (lane == 0) {
+      double *p = part + ((bh * nslot + nslot - 1) * V + v) * 2;
+      p[0] = m;
+      p[1] = l;
+    }
+  }
 }
 
 // Scores of V > 4 score rows per KV head. The fp64 MFMA's operands swap roles
@@ -546,7 +601,7 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
                                                             double *__restrict__ zspill,
                                                             double *__restrict__ part,
                                                             int Hkv, int V, int nvg,
-                                                            int64_t S_pad, int nchunk,
+                                                            int64_t S_pad, int nslot,
                                                             double scale) {
   constexpr int ELT = BF16 ? 2 : 4;
   constexpr int EPP = 16 / ELT;                 // elements per 16-byte piece
@@ -662,7 +717,7 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
   if (j == 0) red2[wave][slot] = v;
   __syncthreads();
   if (wave == 0 && j == 0 && vz < V) {
-    double *p = part + ((bh * nchunk + chunk) * V + vz) * 2;
+    double *p = part + ((bh * nslot + chunk) * V + vz) * 2;
     p[0] = mc;
     p[1] = ((red2[0][slot] + red2[1][slot]) + red2[2][slot]) + red2[3][slot];
   }
@@ -677,7 +732,7 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
                                                         const double *__restrict__ part,
                                                         uint64_t *__restrict__ keys,
                                                         uint32_t *__restrict__ hist, int Hkv,
-                                                        int V, int64_t S_pad, int nchunk,
+                                                        int V, int64_t S_pad, int nslot,
                                                         int64_t max_len) {
   __shared__ uint32_t sh_hist[kHistBins];
   __shared__ double sm[kMaxScoreRows], sinv[kMaxScoreRows];
@@ -693,8 +748,9 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
   // every workgroup of this (b, h) merges the same partials in the same order
   for (int v = wave; v < V; v += 4) {
     double m = -INFINITY, l = 0.0;
-    for (int c = lane; c < nch; c += 64) {
-      const double *p = part + ((bh * nchunk + c) * V + v) * 2;
+    for (int c = lane; c <= nch; c += 64) {
+      const int slot = c < nch ? c : nslot - 1;  // the chunks, then the tail
+      const double *p = part + ((bh * nslot + slot) * V + v) * 2;
       merge_ml(m, l, p[0], p[1]);
     }
 #pragma unroll
@@ -960,74 +1016,81 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
 
 template <int D, int G, bool BF16>
 hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView &kv,
-                           int Hq, int Hkv, const int32_t *k_per_seq, int k_max,
-                           int32_t *idx_out, const SelectWs &ws, hipStream_t stream) {
+                           int Hq, int Hkv, const void *tail, int n_tail,
+                           const int32_t *k_per_seq, int k_max, int32_t *idx_out,
+                           const SelectWs &ws, hipStream_t stream) {
   const double scale = 1.0 / sqrt((double)D);
+  const int nslot = ws.nchunk + 1;  // partial slots per (b, h): chunks, then the tail
   repq_kernel<D, G, BF16><<<dim3(Hkv, batch, (D * G + 255) / 256), 256, 0, stream>>>(
-      q_sel, ws.qbar, ws.hist, block, Hq, Hkv);
+      q_sel, ws.qbar, ws.hist, ws.part, nslot, block, Hq, Hkv);
+  if (n_tail > 0)
+    tail_kernel<BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(ws.qbar, tail, n_tail, ws.part,
+                                                          nslot, Hkv, G, D, scale);
   const dim3 grid(ws.nchunk, Hkv, batch);
   if constexpr (G <= 4) {
     if (kv.pt)
       score_mfma_kernel<D, G, BF16, true><<<grid, 256, 0, stream>>>(
-          kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+          kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, nslot, scale);
     else
       score_mfma_kernel<D, G, BF16, false><<<grid, 256, 0, stream>>>(
-          kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+          kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, nslot, scale);
   } else {
     if (kv.pt)
       score_kernel<D, G, BF16, true><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
-                                                               Hkv, ws.S_pad, ws.nchunk, scale);
+                                                               Hkv, ws.S_pad, nslot, scale);
     else
       score_kernel<D, G, BF16, false><<<grid, 256, 0, stream>>>(kv, ws.qbar, ws.espill, ws.part,
-                                                                Hkv, ws.S_pad, ws.nchunk, scale);
+                                                                Hkv, ws.S_pad, nslot, scale);
   }
   norm_kernel<G><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist,
-                                           Hkv, ws.S_pad, ws.nchunk, kv.max_len);
+                                           Hkv, ws.S_pad, nslot, kv.max_len);
   topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
       kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
   return hipGetLastError();
 }
 
-
 template <int D, int V, bool BF16>
 void launch_score_norm_small(const KvView &kv, int batch, int Hkv, const SelectWs &ws,
-                             double scale, hipStream_t stream) {
+                             int nslot, double scale, hipStream_t stream) {
   const dim3 grid(ws.nchunk, Hkv, batch);
   if (kv.pt)
     score_mfma_kernel<D, V, BF16, true><<<grid, 256, 0, stream>>>(
-        kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+        kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, nslot, scale);
   else
     score_mfma_kernel<D, V, BF16, false><<<grid, 256, 0, stream>>>(
-        kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, ws.nchunk, scale);
+        kv, ws.qbar, ws.espill, ws.part, Hkv, ws.S_pad, nslot, scale);
   norm_kernel<V><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv,
-                                           ws.S_pad, ws.nchunk, kv.max_len);
+                                           ws.S_pad, nslot, kv.max_len);
 }
 
 template <int D, bool BF16>
 hipError_t launch_select_xq_t(int batch, int block, int x, const void *q_sel,
-                              const KvView &kv, int Hq, int Hkv, const int32_t *k_per_seq,
-                              int k_max, int32_t *idx_out, const SelectWs &ws,
-                              hipStream_t stream) {
+                              const KvView &kv, int Hq, int Hkv, const void *tail, int n_tail,
+                              const int32_t *k_per_seq, int k_max, int32_t *idx_out,
+                              const SelectWs &ws, hipStream_t stream) {
   const int V = x * (Hq / Hkv);
   const double scale = 1.0 / sqrt((double)D);
+  const int nslot = ws.nchunk + 1;
   const int zb = min((D * V + 255) / 256, 64);
-  rows_kernel<BF16><<<dim3(Hkv, batch, zb), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist, block,
-                                                             x, Hq, Hkv, D);
-  if (V == 1) launch_score_norm_small<D, 1, BF16>(kv, batch, Hkv, ws, scale, stream);
-  else if (V == 2) launch_score_norm_small<D, 2, BF16>(kv, batch, Hkv, ws, scale, stream);
-  else if (V == 4) launch_score_norm_small<D, 4, BF16>(kv, batch, Hkv, ws, scale, stream);
+  rows_kernel<BF16><<<dim3(Hkv, batch, zb), 256, 0, stream>>>(q_sel, ws.qbar, ws.hist, ws.part,
+                                                             nslot, block, x, Hq, Hkv, D);
+  if (n_tail > 0)
+    tail_kernel<BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(ws.qbar, tail, n_tail, ws.part,
+                                                          nslot, Hkv, V, D, scale);
+  if (V == 1) launch_score_norm_small<D, 1, BF16>(kv, batch, Hkv, ws, nslot, scale, stream);
+  else if (V == 2) launch_score_norm_small<D, 2, BF16>(kv, batch, Hkv, ws, nslot, scale, stream);
+  else if (V == 4) launch_score_norm_small<D, 4, BF16>(kv, batch, Hkv, ws, nslot, scale, stream);
   else {
     const int nvg = (V + 15) / 16;
     const dim3 grid_s(ws.nchunk * nvg, Hkv, batch);
     if (kv.pt)
       score_rows_kernel<D, BF16, true><<<grid_s, 256, 0, stream>>>(
-          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, ws.nchunk, scale);
+          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, nslot, scale);
     else
       score_rows_kernel<D, BF16, false><<<grid_s, 256, 0, stream>>>(
-          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, ws.nchunk, scale);
+          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, nslot, scale);
     norm_rows_kernel<<<dim3(ws.nchunk, Hkv, batch), 256, 0, stream>>>(
-        kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv, V, ws.S_pad, ws.nchunk,
-        kv.max_len);
+        kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv, V, ws.S_pad, nslot, kv.max_len);
   }
   topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
       kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
@@ -1047,7 +1110,7 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
   size_t off = 0;
   const size_t o_qbar = off; off = align256(off + bh * d * G * sizeof(double));
   const size_t o_z = off;    off = align256(off + bh * S_pad * G * sizeof(double));
-  const size_t o_part = off; off = align256(off + bh * nchunk * G * 2 * sizeof(double));
+  const size_t o_part = off; off = align256(off + bh * (nchunk + 1) * G * 2 * sizeof(double));
   const size_t o_keys = off; off = align256(off + bh * S_pad * sizeof(uint64_t));
   const size_t o_hist = off; off = align256(off + bh * kHistBins * sizeof(uint32_t));
   if (layout) {
@@ -1063,26 +1126,22 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
 }
 
 hipError_t launch_select_xq(const herald_heads &hd, int batch, int block, int x,
-                            const void *q_sel, const KvView &kv, const int32_t *k_per_seq,
-                            int k_max, int32_t *idx_out, const SelectWs &ws,
-                            hipStream_t stream) {
+                            const void *q_sel, const KvView &kv, const void *tail, int n_tail,
+                            const int32_t *k_per_seq, int k_max, int32_t *idx_out,
+                            const SelectWs &ws, hipStream_t stream) {
   const bool bf = hd.dtype == HERALD_BF16;
   const int Hq = hd.num_q_heads, Hkv = hd.num_kv_heads;
-  if (hd.head_dim == 64)
-    return bf ? launch_select_xq_t<64, true>(batch, block, x, q_sel, kv, Hq, Hkv, k_per_seq,
-                                             k_max, idx_out, ws, stream)
-              : launch_select_xq_t<64, false>(batch, block, x, q_sel, kv, Hq, Hkv, k_per_seq,
-                                              k_max, idx_out, ws, stream);
-  if (hd.head_dim == 128)
-    return bf ? launch_select_xq_t<128, true>(batch, block, x, q_sel, kv, Hq, Hkv, k_per_seq,
-                                              k_max, idx_out, ws, stream)
-              : launch_select_xq_t<128, false>(batch, block, x, q_sel, kv, Hq, Hkv,
-                                               k_per_seq, k_max, idx_out, ws, stream);
+#define HERALD_SELX(D_, BF_)                                                              \
+  if (hd.head_dim == D_ && bf == BF_)                                                     \
+    return launch_select_xq_t<D_, BF_>(batch, block, x, q_sel, kv, Hq, Hkv, tail, n_tail, \
+                                       k_per_seq, k_max, idx_out, ws, stream);
+  HERALD_SELX(64, true) HERALD_SELX(64, false) HERALD_SELX(128, true) HERALD_SELX(128, false)
+#undef HERALD_SELX
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_select(const herald_heads &hd, int batch, int block, const void *q_sel,
-                         const KvView &kv, int64_t /*max_seq_len*/,
+                         const KvView &kv, const void *tail, int n_tail,
                          const int32_t *k_per_seq, int k_max, int32_t *idx_out,
                          const SelectWs &ws, hipStream_t stream) {
   const int G = hd.num_q_heads / hd.num_kv_heads;
@@ -1090,10 +1149,12 @@ hipError_t launch_select(const herald_heads &hd, int batch, int block, const voi
   const int Hq = hd.num_q_heads, Hkv = hd.num_kv_heads;
 #define HERALD_SEL(D_, G_)                                                              \
   if (hd.head_dim == D_ && G == G_)                                                     \
-    return bf ? launch_select_t<D_, G_, true>(batch, block, q_sel, kv, Hq, Hkv,         \
-                                              k_per_seq, k_max, idx_out, ws, stream)   \
-              : launch_select_t<D_, G_, false>(batch, block, q_sel, kv, Hq, Hkv,        \
-                                               k_per_seq, k_max, idx_out, ws, stream);
+    return bf ? launch_select_t<D_, G_, true>(batch, block, q_sel, kv, Hq, Hkv, tail,   \
+                                              n_tail, k_per_seq, k_max, idx_out, ws,    \
+                                              stream)                                   \
+              : launch_select_t<D_, G_, false>(batch, block, q_sel, kv, Hq, Hkv, tail,  \
+                                               n_tail, k_per_seq, k_max, idx_out, ws,   \
+                                               stream);
   HERALD_SEL(64, 1) HERALD_SEL(64, 2) HERALD_SEL(64, 4) HERALD_SEL(64, 8)
   HERALD_SEL(128, 1) HERALD_SEL(128, 2) HERALD_SEL(128, 4) HERALD_SEL(128, 8)
 #undef HERALD_SEL

@@ -81,6 +81,10 @@ def lib():
     L.herald_select_xq.restype = ctypes.c_int
     L.herald_select_xq.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i32, c_p,
                                    ctypes.POINTER(KV), c_p, c_i32, c_p, c_p, c_sz, c_p]
+    L.herald_select_draft.restype = ctypes.c_int
+    L.herald_select_draft.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i32, c_p,
+                                      ctypes.POINTER(KV), c_p, c_i32, c_p, c_i32, c_p, c_p,
+                                      c_sz, c_p]
     L.herald_gather.restype = ctypes.c_int
     L.herald_gather.argtypes = [ctypes.POINTER(Heads), c_i32, ctypes.POINTER(KV), c_p, c_p,
                                 c_i32, ctypes.POINTER(Pool), c_i32, c_p]
@@ -89,6 +93,9 @@ def lib():
     L.herald_block_attn.restype = ctypes.c_int
     L.herald_block_attn.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_p,
                                     ctypes.POINTER(KV), c_p, c_p, c_p, c_p, c_sz, c_p]
+    L.herald_block_attn_groups.restype = ctypes.c_int
+    L.herald_block_attn_groups.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i32, c_p,
+                                           ctypes.POINTER(KV), c_p, c_p, c_p, c_p, c_sz, c_p]
     L.herald_decode_block_workspace.restype = c_sz
     L.herald_decode_block_workspace.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i64,
                                                 c_i32]
@@ -102,8 +109,10 @@ def lib():
 
 EXPORTS = ("herald_status_string", "herald_budget_tokens", "herald_select_workspace",
            "herald_select", "herald_select_xq_workspace", "herald_select_xq",
+           "herald_select_draft",
            "herald_gather", "herald_block_attn_workspace",
-           "herald_block_attn", "herald_decode_block_workspace", "herald_decode_block")
+           "herald_block_attn", "herald_block_attn_groups", "herald_decode_block_workspace",
+           "herald_decode_block")
 
 
 # ------------------------------------------------------------------ helpers
@@ -160,12 +169,16 @@ def kv_view(k, v, seq_lens, max_seq_len: int, page_table=None) -> KV:
         kv.page_table = _ptr(page_table)
         kv.page_size = k.shape[2]
         kv.max_pages = page_table.shape[1]
+    # the view holds raw device pointers: keep the tensors alive with it
+    kv._refs = (k, v, seq_lens, page_table)
     return kv
 
 
 def pool_view(k, v) -> Pool:
     """Writable view of [batch][Hkv][capacity][d] tensors."""
-    return Pool(_ptr(k), _ptr(v), k.stride(0), k.stride(1), k.stride(2), k.shape[2])
+    pool = Pool(_ptr(k), _ptr(v), k.stride(0), k.stride(1), k.stride(2), k.shape[2])
+    pool._refs = (k, v)  # keep the tensors alive with the view
+    return pool
 
 
 # ------------------------------------------------------------------ entry points
@@ -201,6 +214,15 @@ def select_xq(hd: Heads, batch: int, block: int, x: int, q_sel, kv: KV, k_per_se
     _check("herald_select_xq", st)
 
 
+def select_draft(hd: Heads, batch: int, block: int, x: int, q_sel, kv: KV, draft_k, n_draft: int,
+                 k_per_seq, k_max: int, idx_out, ws, ws_bytes: int | None = None, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().herald_select_draft(ctypes.byref(hd), batch, block, x, _ptr(q_sel),
+                                   ctypes.byref(kv), _ptr(draft_k), n_draft, _ptr(k_per_seq),
+                                   k_max, _ptr(idx_out), _ptr(ws), nbytes, _stream(stream))
+    _check("herald_select_draft", st)
+
+
 def gather(hd: Heads, batch: int, kv: KV, idx, k_per_seq, k_max: int, dst: Pool,
            dst_row0: int = 0, stream=None):
     st = lib().herald_gather(ctypes.byref(hd), batch, ctypes.byref(kv), _ptr(idx),
@@ -221,6 +243,16 @@ def block_attn(hd: Heads, batch: int, block: int, q, ctx: KV, blk_k, blk_v, out,
                                  _ptr(blk_k), _ptr(blk_v), _ptr(out), _ptr(ws), nbytes,
                                  _stream(stream))
     _check("herald_block_attn", st)
+
+
+def block_attn_groups(hd: Heads, batch: int, block: int, groups: int, q, ctx: KV, blk_k, blk_v,
+                      out, ws, ws_bytes: int | None = None, stream=None):
+    nbytes = (ws.numel() * ws.element_size() if ws is not None else 0) \
+        if ws_bytes is None else ws_bytes
+    st = lib().herald_block_attn_groups(ctypes.byref(hd), batch, block, groups, _ptr(q),
+                                        ctypes.byref(ctx), _ptr(blk_k), _ptr(blk_v), _ptr(out),
+                                        _ptr(ws), nbytes, _stream(stream))
+    _check("herald_block_attn_groups", st)
 
 
 def decode_block_workspace(hd: Heads, batch: int, block: int, max_seq_len: int,

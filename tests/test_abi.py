@@ -126,6 +126,48 @@ def test_select_xq_validation():
     assert _select_xq(hd=H.heads(32, 8, 96, "bf16")) == H.ERR_UNSUPPORTED
 
 
+def _select_draft(x=0, draft=FAKE, n_draft=32, batch=2, block=32, ws_bytes=None, **kw):
+    hd = H.heads(32, 8, 128, "bf16")
+    kv = _kv()
+    if ws_bytes is None:
+        ws_bytes = H.select_xq_workspace(hd, batch, max(x, 1), kv.max_seq_len) - 1
+    return H.lib().herald_select_draft(ctypes.byref(hd), batch, block, x, FAKE,
+                                       ctypes.byref(kv), draft, n_draft, FAKE, 52, FAKE,
+                                       FAKE * 256, ws_bytes, None)
+
+
+def test_select_draft_validation():
+    assert _select_draft() == H.ERR_WORKSPACE                     # one byte short
+    assert _select_draft(x=2) == H.ERR_WORKSPACE
+    assert _select_draft(x=-1, ws_bytes=1 << 40) == H.ERR_INVALID_ARG
+    assert _select_draft(x=33, ws_bytes=1 << 40) == H.ERR_INVALID_ARG   # x > block
+    assert _select_draft(n_draft=-1, ws_bytes=1 << 40) == H.ERR_INVALID_ARG
+    assert _select_draft(n_draft=65, ws_bytes=1 << 40) == H.ERR_INVALID_ARG
+    assert _select_draft(draft=None, ws_bytes=1 << 40) == H.ERR_INVALID_ARG
+    assert _select_draft(draft=FAKE + 4, ws_bytes=1 << 40) == H.ERR_INVALID_ARG
+    assert _select_draft(draft=None, n_draft=0) == H.ERR_WORKSPACE  # no draft: fine to here
+
+
+def test_block_attn_groups_validation():
+    hd = H.heads(32, 8, 128, "bf16")
+    kv = _kv(max_seq_len=1638)
+
+    def call(groups, ws=None, ws_bytes=0, q=FAKE, batch=16):
+        return H.lib().herald_block_attn_groups(ctypes.byref(hd), batch, 32, groups, q,
+                                                ctypes.byref(kv), FAKE, FAKE, FAKE, ws,
+                                                ws_bytes, None)
+    assert call(0) == H.ERR_INVALID_ARG
+    assert call(-2) == H.ERR_INVALID_ARG
+    assert call(2, q=FAKE + 8) == H.ERR_INVALID_ARG
+    # one sequence, two groups: the key range is split, and the partials are
+    # sized for batch * groups = 2 blocks, more than for one block
+    need = H.block_attn_workspace(hd, 2, 32, 1638)
+    small = H.block_attn_workspace(hd, 1, 32, 1638)
+    assert need > small > 256                     # so the call below fails the size check
+    assert call(2, ws=FAKE * 256, ws_bytes=small, batch=1) == H.ERR_WORKSPACE
+    assert call(2, ws=None, ws_bytes=1 << 40, batch=1) == H.ERR_WORKSPACE
+
+
 def test_select_xq_workspace_grows_with_x():
     hd = H.heads(32, 8, 128, "bf16")
     w = [H.select_xq_workspace(hd, 16, x, 32768) for x in (1, 2, 4, 8, 16, 32)]

@@ -106,3 +106,53 @@ def test_attn_bf16_layer_32k_pool_shape():
 def test_attn_bf16_dense_over_full_cache_shape():
     """Dense attention (the 100%-budget baseline) over 65536 cached rows."""
     run_attn("bf16", 2, 32, 8, 128, 32, [65536, 40000], seed=10)
+
+
+def run_attn_groups(dtype, batch, groups, Hq, Hkv, d, block, n_ctx, seed=0, seqs=None):
+    """groups query groups per sequence over one shared context, each with its
+    own block KV: GPU herald_block_attn_groups vs oracle.attn_groups."""
+    rng = np.random.default_rng(seed)
+    n_ctx = np.asarray(n_ctx, np.int32)
+    cap = max(1, int(n_ctx.max()))
+
+    def rnd(shape):
+        x = rng.standard_normal(shape).astype(np.float32)
+        return synth._to_dtype(x, dtype)
+    nb = groups * block
+    q = rnd((batch, nb, Hq, d))
+    ck = rnd((batch, Hkv, cap, d))
+    cv = rnd((batch, Hkv, cap, d))
+    bk = rnd((batch, nb, Hkv, d))
+    bv = rnd((batch, nb, Hkv, d))
+    hd = H.heads(Hq, Hkv, d, dtype)
+    tq, tck, tcv, tbk, tbv = map(to_dev, (q, ck, cv, bk, bv))
+    lens = to_dev(n_ctx)  # the view holds its device pointer: keep it alive
+    ctx = H.kv_view(tck, tcv, lens, int(n_ctx.max()))
+    out = torch.zeros_like(tq)
+    ws = H.workspace(H.block_attn_workspace(hd, batch * groups, block, int(n_ctx.max())), DEV)
+    H.block_attn_groups(hd, batch, block, groups, tq, ctx, tbk, tbv, out, ws)
+    torch.cuda.synchronize()
+    got = f64(to_host(out))
+    worst = 0.0
+    for b in (range(batch) if seqs is None else seqs):
+        n = int(n_ctx[b])
+        want = oracle.attn_groups(q[b], ck[b, :, :n], cv[b, :, :n], bk[b], bv[b], groups)
+        err = float(np.abs(got[b] - want).max())
+        worst = max(worst, err)
+        assert err <= TOL[dtype], f"seq {b} (n_ctx={n}): max abs err {err}"
+    print(f"[attn groups] {dtype} b={batch} groups={groups} d={d} B={block}: max abs err {worst:.3g}")
+    return worst
+
+
+@pytest.mark.parametrize("dtype,groups,block,n_ctx", [
+    ("bf16", 2, 32, [1638, 0, 700]), ("bf16", 3, 16, [5000, 64, 1]), ("bf16", 2, 4, [300, 31]),
+    ("f32", 2, 4, [209, 0]), ("f32", 3, 8, [700, 65, 1])])
+def test_attn_groups_share_the_context_not_each_other(dtype, groups, block, n_ctx):
+    d = 128 if dtype == "bf16" else 64
+    run_attn_groups(dtype, len(n_ctx), groups, 8, 2, d, block, n_ctx, seed=groups * 10 + block)
+
+
+def test_attn_groups_layer_32k_draft_step_shape():
+    """The 2B-token step of the 8B-class layer: denoising and draft groups of
+    32 queries over the 1638-row pool; 3 sequences checked by the oracle."""
+    run_attn_groups("bf16", 16, 2, 32, 8, 128, 32, [1638] * 16, seed=12, seqs=[0, 7, 15])

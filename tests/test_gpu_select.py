@@ -7,6 +7,7 @@ import pytest
 import torch
 
 import oracle
+from paper_2606_21633_amd import herald as H
 from paper_2606_21633_amd import synth
 from tests.gpu_util import (DEV, Staged, assert_same_selection, boundary_gap, budgets,
                             seq_kv_host, to_dev)
@@ -205,6 +206,63 @@ def test_select_xq_layer_32k_sampled(x, seqs):
     """The 8B-class 32K layer as the x sweep runs it (all 16 sequences on the
     GPU in one call), sampled sequences checked by the oracle."""
     assert check_select_xq(synth.LAYER_32K, x, seqs=seqs) == 0
+
+
+# ---------------------------------------------------------------- draft tail
+
+
+def check_select_draft(wl, x, n_draft, scale=2.0, seqs=None, seed=5):
+    inp = synth.make_host(wl)
+    rng = np.random.default_rng(seed)
+    st = Staged(wl, inp)
+    lens = inp["seq_lens"]
+    kps_h = budgets(lens, *wl.budget)
+    k_max = int(max(1, min(kps_h.max(), lens.max())))
+    d = wl.head_dim
+    draft = synth._to_dtype((rng.standard_normal((wl.batch, max(n_draft, 1), wl.num_kv_heads, d))
+                             * scale).astype(np.float32), wl.dtype)
+    kps = to_dev(kps_h)
+    idx = torch.full((wl.batch, wl.num_kv_heads, k_max), -7, dtype=torch.int32, device=DEV)
+    ws = H.workspace(H.select_xq_workspace(st.hd, wl.batch, max(x, 1), st.S_max), DEV)
+    tdraft = to_dev(draft)
+    H.select_draft(st.hd, wl.batch, wl.block, x, st.q_sel, st.kv, tdraft, n_draft, kps,
+                   k_max, idx, ws)
+    torch.cuda.synchronize()
+    got = idx.cpu().numpy()
+    near = 0
+    for b in (range(wl.batch) if seqs is None else seqs):
+        S = int(lens[b])
+        k = int(min(max(kps_h[b], 0), S, k_max))
+        assert (got[b, :, k:] == -1).all()
+        kh, _ = seq_kv_host(inp, b)
+        tail = draft[b, :n_draft] if n_draft > 0 else None
+        idx_o, shat = oracle.select_draft(inp["q_sel"][b], kh, tail, k, x)
+        for h in range(wl.num_kv_heads):
+            near += assert_same_selection(got[b, h, :k], idx_o[h], shat[h], k)
+    print(f"[select_draft] {wl.name} x={x} n_draft={n_draft}: near-ties={near}")
+    return near, got
+
+
+@pytest.mark.parametrize("x,n_draft", [(0, 32), (1, 32), (0, 0), (1, 1), (3, 64), (8, 32)])
+def test_select_draft_tail(x, n_draft):
+    wl = XQ.replace(name=f"draft x{x}", num_q_heads=8, seed=80 + x + n_draft)
+    assert check_select_draft(wl, x, n_draft)[0] == 0
+
+
+@pytest.mark.parametrize("G,d,dtype", [(1, 64, "f32"), (8, 128, "bf16"), (2, 64, "bf16")])
+def test_select_draft_group_and_dims(G, d, dtype):
+    wl = XQ.replace(name=f"draft G{G} d{d} {dtype}", num_q_heads=2 * G, head_dim=d, dtype=dtype,
+                    seed=90 + G + d)
+    assert check_select_draft(wl, 0, 16)[0] == 0
+
+
+def test_select_draft_paged_and_strong_draft_changes_selection():
+    wl = XQ.replace(name="draft paged", batch=4, page_size=16, seq_len=3000, seq_len_lo=17,
+                    num_q_heads=8, seed=33)
+    near, with_d = check_select_draft(wl, 1, 32, scale=8.0)
+    assert near == 0
+    _, without = check_select_draft(wl, 1, 0)
+    assert (with_d != without).any()
 
 
 def test_select_layer_32k_workload_full():
