@@ -276,6 +276,17 @@ typedef struct {
   int32_t dense;        /* nonzero: this layer keeps exact attention over its
                            full cache (the paper keeps its first layers so,
                            sec. IV-B.2); it has no pools and no selection  */
+  /* Draft-based lookahead (sec. IV-A.1, sec. IV-B.2): NULL q_draft = none.
+   * With a draft, step 1 is the 2B-token step: the draft group (q_draft over
+   * the same context, with draft_k/draft_v as its own block KV) runs beside
+   * the denoising group, and the next block's selection waits for it and
+   * takes draft_k as a normalisation tail (herald_select_draft). */
+  const void *q_draft;  /* [batch][block][H_q][d] draft group's queries    */
+  const void *draft_k;  /* [batch][block][H_kv][d] the draft's K            */
+  const void *draft_v;  /* [batch][block][H_kv][d] the draft's V            */
+  void *out_draft;      /* [batch][block][H_q][d] draft group's output      */
+  int32_t select_x;     /* next block's representative query: 0 the mean of
+                           q_next, 1 its centre row (the paper's choice)     */
 } herald_layer;
 
 /* Workspace bytes needed by herald_decode_block (0 if invalid). */
@@ -300,7 +311,15 @@ size_t herald_decode_block_workspace(const herald_heads *heads,
  * != 0 the main stream attends over the full cache (rows [0, S_n)) instead of
  * the pool and no selection runs (the GPU-only dense baseline); the append
  * still runs. A layer whose own dense flag is set is treated so in any case
- * (its active and idle pools are not read and may be null views). Everything is ordered on s_main when the call's work ends; the
+ * (its active and idle pools are not read and may be null views).
+ * Draft lookahead: if any layer has a q_draft, step 1 of those layers also
+ * runs their draft group (q_draft over the same context with draft_k/draft_v
+ * as its block KV, output out_draft), and the retrieval stream starts only
+ * after step 1 of every layer (the draft is that step's product, sec. IV-B.2
+ * steps 3 and 7); each such layer's selection then takes draft_k as its
+ * normalisation tail (herald_select_draft); steps must be >= 2. select_x
+ * picks the representative (0: mean of q_next, 1: its centre row).
+ * Everything is ordered on s_main when the call's work ends; the
  * retrieval stream first waits for work already enqueued on s_main. k_next
  * (device [batch]) is the next pool's budget; k_max bounds it and
  * k_max + block <= idle.capacity. The cache capacity must hold S_n + block.

@@ -245,7 +245,8 @@ def attn(q, ctx_k, ctx_v, blk_k, blk_v):
     return out
 
 
-def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20, x: int = 0):
+def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20, x: int = 0,
+                  draft_outs: list | None = None):
     """Sequential schedule of consecutive blocks of one sequence, one layer.
 
     K0, V0 [Hkv][S0][d]: the prefix cache before the first block.
@@ -258,6 +259,9 @@ def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20, x: int
     Optional per block: k_draft [B][Hkv][d], block n's draft KV, which block
     n+1's selection appends for normalisation (sec. IV-B.2, steps 7-8);
     x = 0 selects with the mean of q_next, x >= 1 with its x centred rows.
+    With q_draft [B][Hq][d] and v_draft as well, the draft group of the
+    2B-token step attends to pool(n) and its own draft KV; its output is
+    appended to draft_outs (None for blocks without a draft) if given.
     Block n is denoised over pool(n); block n+1's selection runs over the
     prefix before block n; pool(n+1) = that top-k followed by block n's
     completed KV; then the cache grows by block n's completed KV.
@@ -273,6 +277,9 @@ def decode_blocks(K0, V0, pool_idx0, blocks, num: int = 1, den: int = 20, x: int
         outs.append(np.stack([attn(blk["q_steps"][t], pool_k, pool_v,
                                    blk["k_steps"][t], blk["v_steps"][t])
                               for t in range(T)]))
+        if draft_outs is not None:
+            draft_outs.append(attn(blk["q_draft"], pool_k, pool_v, blk["k_draft"], blk["v_draft"])
+                              if blk.get("q_draft") is not None else None)
         S = Kc.shape[1]
         k = budget(S, num, den)
         if x == 0 and blk.get("k_draft") is None:

@@ -312,7 +312,16 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
     for (const void *p : ptrs)
       if (!p || !aligned16(p)) return HERALD_ERR_INVALID_ARG;
     if (L.out_step_stride < 0 || !stride_ok(L.out_step_stride, elt)) return HERALD_ERR_INVALID_ARG;
+    if (L.select_x != 0 && L.select_x != 1) return HERALD_ERR_INVALID_ARG;
+    if (L.q_draft) {
+      const void *dp[4] = {L.q_draft, L.draft_k, L.draft_v, L.out_draft};
+      for (const void *p : dp)
+        if (!p || !aligned16(p)) return HERALD_ERR_INVALID_ARG;
+      if (steps < 2) return HERALD_ERR_INVALID_ARG;  // the draft runs with step 1
+    }
   }
+  bool any_draft = false;
+  for (int l = 0; l < num_layers; ++l) any_draft = any_draft || layers[l].q_draft != nullptr;
   const size_t need = herald_decode_block_workspace(heads, batch, block, max_seq_len,
                                                     any_sparse ? k_max : 1);
   if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
@@ -332,29 +341,39 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
   const int64_t q_step = (int64_t)batch * block * Hq * D;   // elements per step
   const int64_t kv_step = (int64_t)batch * block * Hkv * D;
 
-  hipEvent_t ev_start = nullptr, ev_sel = nullptr;
+  hipEvent_t ev_start = nullptr, ev_sel = nullptr, ev_draft = nullptr;
   hipError_t e = hipEventCreateWithFlags(&ev_start, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&ev_sel, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&ev_draft, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventRecord(ev_start, s_main);
-  if (e == hipSuccess && any_sparse) e = hipStreamWaitEvent(s_retr, ev_start, 0);
 
-  // retrieval stream: next block's selection + gather into the idle pools
-  if (e == hipSuccess && any_sparse) {
-    for (int l = 0; l < num_layers && e == hipSuccess; ++l) {
+  // retrieval stream, once `after` has been reached on the main stream: the
+  // next block's selection (with the layer's draft as normalisation tail, if
+  // it has one) and the gather into the idle pools
+  auto retrieval = [&](hipEvent_t after) -> hipError_t {
+    hipError_t r = hipStreamWaitEvent(s_retr, after, 0);
+    for (int l = 0; l < num_layers && r == hipSuccess; ++l) {
       if (layer_dense(l)) continue;
       const herald_layer &L = layers[l];
       herald_kv cache = kv_of_pool(&L.cache, seq_lens, max_seq_len);
-      e = launch_select(*heads, batch, block, L.q_next, view_of(&cache), nullptr, 0, k_next,
-                        k_max, idx, sel, s_retr);
-      if (e == hipSuccess)
-        e = launch_gather(*heads, batch, view_of(&cache), idx, k_next, k_max, pool_of(&L.idle),
+      const void *tail = L.q_draft ? L.draft_k : nullptr;
+      const int n_tail = L.q_draft ? block : 0;
+      r = L.select_x == 0
+              ? launch_select(*heads, batch, block, L.q_next, view_of(&cache), tail, n_tail,
+                              k_next, k_max, idx, sel, s_retr)
+              : launch_select_xq(*heads, batch, block, 1, L.q_next, view_of(&cache), tail,
+                                 n_tail, k_next, k_max, idx, sel, s_retr);
+      if (r == hipSuccess)
+        r = launch_gather(*heads, batch, view_of(&cache), idx, k_next, k_max, pool_of(&L.idle),
                           0, s_retr);
     }
-    if (e == hipSuccess) e = hipEventRecord(ev_sel, s_retr);
-  }
-  // main stream: T denoising steps over every layer
-  for (int t = 0; t < steps && e == hipSuccess; ++t) {
-    for (int l = 0; l < num_layers && e == hipSuccess; ++l) {
+    if (r == hipSuccess) r = hipEventRecord(ev_sel, s_retr);
+    return r;
+  };
+  // main stream: denoising step t of every layer (step 1 with the draft group)
+  auto step = [&](int t) -> hipError_t {
+    hipError_t r = hipSuccess;
+    for (int l = 0; l < num_layers && r == hipSuccess; ++l) {
       const herald_layer &L = layers[l];
       herald_kv ctx = layer_dense(l) ? kv_of_pool(&L.cache, seq_lens, max_seq_len)
                                      : kv_of_pool(&L.active, n_active, max_active);
@@ -362,9 +381,24 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
       const char *bk = reinterpret_cast<const char *>(L.blk_k) + t * kv_step * elt;
       const char *bv = reinterpret_cast<const char *>(L.blk_v) + t * kv_step * elt;
       char *o = reinterpret_cast<char *>(L.out) + t * L.out_step_stride * elt;
-      e = launch_block_attn(*heads, batch, block, 1, q, view_of(&ctx), ctx.max_seq_len, bk, bv, o,
-                            attn_ws, s_main);
+      r = launch_block_attn(*heads, batch, block, 1, q, view_of(&ctx), ctx.max_seq_len, bk, bv,
+                            o, attn_ws, s_main);
+      if (r == hipSuccess && t == 1 && L.q_draft)
+        r = launch_block_attn(*heads, batch, block, 1, L.q_draft, view_of(&ctx),
+                              ctx.max_seq_len, L.draft_k, L.draft_v, L.out_draft, attn_ws,
+                              s_main);
     }
+    return r;
+  };
+  if (!any_draft) {
+    if (e == hipSuccess && any_sparse) e = retrieval(ev_start);
+    for (int t = 0; t < steps && e == hipSuccess; ++t) e = step(t);
+  } else {
+    // the selection needs the draft, which the 2B-token step 1 produces
+    for (int t = 0; t < 2 && e == hipSuccess; ++t) e = step(t);
+    if (e == hipSuccess) e = hipEventRecord(ev_draft, s_main);
+    if (e == hipSuccess && any_sparse) e = retrieval(ev_draft);
+    for (int t = 2; t < steps && e == hipSuccess; ++t) e = step(t);
   }
   // join, append the completed block, advance the lengths
   if (e == hipSuccess && any_sparse) e = hipStreamWaitEvent(s_main, ev_sel, 0);
@@ -379,6 +413,7 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
                     s_main);
   if (ev_start) hipEventDestroy(ev_start);
   if (ev_sel) hipEventDestroy(ev_sel);
+  if (ev_draft) hipEventDestroy(ev_draft);
   return hip_status(e);
 }
 

@@ -41,7 +41,8 @@ class Layer(ctypes.Structure):
     _fields_ = [("cache", Pool), ("active", Pool), ("idle", Pool), ("q_steps", c_p),
                 ("blk_k", c_p), ("blk_v", c_p), ("done_k", c_p), ("done_v", c_p),
                 ("q_next", c_p), ("out", c_p), ("out_step_stride", c_i64),
-                ("dense", c_i32)]
+                ("dense", c_i32), ("q_draft", c_p), ("draft_k", c_p), ("draft_v", c_p),
+                ("out_draft", c_p), ("select_x", c_i32)]
 
 
 class HeraldError(RuntimeError):

@@ -239,6 +239,30 @@ def test_decode_block_validation():
     assert call(args(ws=FAKE * 256 + 16)) == H.ERR_WORKSPACE
 
 
+def test_decode_block_draft_fields_are_validated():
+    hd = H.heads(32, 8, 128, "bf16")
+    cache = H.Pool(FAKE, FAKE, 8 * 2048 * 128, 2048 * 128, 128, 2048)
+    pool = H.Pool(FAKE, FAKE, 8 * 200 * 128, 200 * 128, 128, 200)
+
+    def call(steps=4, wsb=10, **fields):
+        lay = H.Layer(cache, pool, pool, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0)
+        for k, v in fields.items():
+            setattr(lay, k, v)
+        arr = (H.Layer * 1)(lay)
+        return H.lib().herald_decode_block(ctypes.byref(hd), 1, 2, 32, steps, arr, FAKE, 2000,
+                                           FAKE, 150, FAKE, FAKE, 100, 0, FAKE * 256, wsb,
+                                           None, None)
+    full = dict(q_draft=FAKE, draft_k=FAKE, draft_v=FAKE, out_draft=FAKE)
+    assert call(**full) == H.ERR_WORKSPACE                      # valid up to the workspace
+    assert call(select_x=1) == H.ERR_WORKSPACE
+    assert call(select_x=2) == H.ERR_INVALID_ARG                # 0 or 1 only
+    assert call(select_x=-1) == H.ERR_INVALID_ARG
+    assert call(steps=1, **full) == H.ERR_INVALID_ARG           # the draft runs with step 1
+    for missing in ("draft_k", "draft_v", "out_draft"):
+        assert call(**dict(full, **{missing: None})) == H.ERR_INVALID_ARG
+    assert call(**dict(full, draft_k=FAKE + 4)) == H.ERR_INVALID_ARG
+
+
 def test_decode_block_dense_layers_need_no_pools():
     """A layer flagged dense keeps no pools: its null pool views pass the
     checks, while the sparse layers beside it are still checked."""

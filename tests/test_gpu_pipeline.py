@@ -24,7 +24,7 @@ TOL = 2e-2
 
 
 def make_case(b=2, Hq=8, Hkv=2, d=128, B=8, T=2, L=2, nblocks=3, S_lo=900, S_hi=1500,
-              seed=1, dtype="bf16"):
+              seed=1, dtype="bf16", drafts=False):
     rng = np.random.default_rng(seed)
     lens = rng.integers(S_lo, S_hi, size=b, endpoint=True).astype(np.int32)
     cap = int(lens.max()) + nblocks * B
@@ -42,12 +42,18 @@ def make_case(b=2, Hq=8, Hkv=2, d=128, B=8, T=2, L=2, nblocks=3, S_lo=900, S_hi=
                        bv=rnd((T, b, B, Hkv, d)), dk=rnd((b, B, Hkv, d)),
                        dvv=rnd((b, B, Hkv, d)), qn=rnd((b, B, Hq, d)))
                   for _ in range(nblocks)]
+        if drafts:
+            for blk in blocks:   # strong draft keys, so that the tail matters
+                blk.update(qd=rnd((b, B, Hq, d)), ddk=synth._to_dtype(
+                    3.0 * rng.standard_normal((b, B, Hkv, d)).astype(np.float32), dtype),
+                    ddv=rnd((b, B, Hkv, d)))
         layers.append(dict(k=k, v=v, q_sel0=rnd((b, B, Hq, d)), blocks=blocks))
     return dict(b=b, Hq=Hq, Hkv=Hkv, d=d, B=B, T=T, L=L, nblocks=nblocks, lens=lens,
                 cap=cap, layers=layers)
 
 
-def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, dense_layers=()):
+def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, dense_layers=(),
+            draft_layers=(), select_x=0):
     b, Hq, Hkv, d, B, T, L = (case[x] for x in ("b", "Hq", "Hkv", "d", "B", "T", "L"))
     hd = H.heads(Hq, Hkv, d, "bf16")
     lens_h = case["lens"].copy()
@@ -62,6 +68,7 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
         L_["pools"] = [[torch.zeros((b, Hkv, pcap, d), dtype=torch.bfloat16, device=DEV)
                         for _ in range(2)] for _ in range(2)]
         L_["out"] = torch.zeros((T, b, B, Hq, d), dtype=torch.bfloat16, device=DEV)
+        L_["out_draft"] = torch.zeros((b, B, Hq, d), dtype=torch.bfloat16, device=DEV)
         L_["blocks"] = [{n: to_dev(a) for n, a in blk.items()} for blk in lay["blocks"]]
         dl.append(L_)
     n_pool = [torch.zeros(b, dtype=torch.int32, device=DEV) for _ in range(2)]
@@ -91,12 +98,17 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
         layers = []
         for l, L_ in enumerate(dl):
             blk = L_["blocks"][n]
-            layers.append(H.Layer(
+            layer = H.Layer(
                 H.pool_view(L_["k"], L_["v"]), H.pool_view(*L_["pools"][a]),
                 H.pool_view(*L_["pools"][1 - a]), blk["q"].data_ptr(), blk["bk"].data_ptr(),
                 blk["bv"].data_ptr(), blk["dk"].data_ptr(), blk["dvv"].data_ptr(),
                 blk["qn"].data_ptr(), L_["out"].data_ptr(), b * B * Hq * d,
-                int(l in dense_layers)))
+                int(l in dense_layers))
+            layer.select_x = select_x
+            if l in draft_layers:
+                layer.q_draft, layer.draft_k = blk["qd"].data_ptr(), blk["ddk"].data_ptr()
+                layer.draft_v, layer.out_draft = blk["ddv"].data_ptr(), L_["out_draft"].data_ptr()
+            layers.append(layer)
         torch.cuda.synchronize()
         if delay_main:
             with torch.cuda.stream(s_main):
@@ -105,6 +117,8 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
                        n_pool[1 - a], kn, int(kn_h.max()), dense, ws, s_main, s_retr)
         torch.cuda.synchronize()
         outs.append([to_host(L_["out"]).copy() for L_ in dl])
+        if draft_layers:
+            outs[-1].append([to_host(L_["out_draft"]).copy() for L_ in dl])
         lens_h = lens_h + B
         assert np.array_equal(lens.cpu().numpy(), lens_h)
         if not dense:
@@ -114,9 +128,11 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
     return outs, caches
 
 
-def oracle_outs(case, num=1, den=20, dense_layers=()):
+def oracle_outs(case, num=1, den=20, dense_layers=(), draft_layers=(), select_x=0):
     """Per layer, per sequence: oracle.decode_blocks -> [block][layer][T][b]...
-    A dense layer is the same schedule at a 100% budget."""
+    A dense layer is the same schedule at a 100% budget. Draft layers carry
+    their draft KV (the next selection's normalisation tail) and draft group
+    (whose outputs go to res[("draft", l, i)])."""
     res = {}
     for l, lay in enumerate(case["layers"]):
         nm, dn = (1, 1) if l in dense_layers else (num, den)
@@ -128,12 +144,21 @@ def oracle_outs(case, num=1, den=20, dense_layers=()):
             blocks = [dict(q_steps=blk["q"][:, i], k_steps=blk["bk"][:, i],
                            v_steps=blk["bv"][:, i], k_done=blk["dk"][i], v_done=blk["dvv"][i],
                            q_next=blk["qn"][i]) for blk in lay["blocks"]]
-            res[(l, i)] = oracle.decode_blocks(K0, V0, idx0, blocks, nm, dn)
+            if l in draft_layers:
+                for blk, src in zip(blocks, lay["blocks"]):
+                    blk.update(q_draft=src["qd"][i], k_draft=src["ddk"][i],
+                               v_draft=src["ddv"][i])
+            douts = []
+            x = select_x if l not in dense_layers else 0
+            res[(l, i)] = oracle.decode_blocks(K0, V0, idx0, blocks, nm, dn, x=x,
+                                               draft_outs=douts)
+            res[("draft", l, i)] = douts
     return res
 
 
-def check_against_oracle(case, outs, num=1, den=20, dense_layers=()):
-    ref = oracle_outs(case, num, den, dense_layers)
+def check_against_oracle(case, outs, num=1, den=20, dense_layers=(), draft_layers=(),
+                         select_x=0):
+    ref = oracle_outs(case, num, den, dense_layers, draft_layers, select_x)
     worst = 0.0
     for n in range(case["nblocks"]):
         for l in range(case["L"]):
@@ -142,6 +167,11 @@ def check_against_oracle(case, outs, num=1, den=20, dense_layers=()):
                 err = float(np.abs(got[:, i] - ref[(l, i)][n]).max())
                 worst = max(worst, err)
                 assert err <= TOL, f"block {n} layer {l} seq {i}: {err}"
+                if l in draft_layers:
+                    gd = f64(outs[n][case["L"]][l])[i]
+                    err = float(np.abs(gd - ref[("draft", l, i)][n]).max())
+                    worst = max(worst, err)
+                    assert err <= TOL, f"draft group, block {n} layer {l} seq {i}: {err}"
     print(f"[pipeline] max abs err {worst:.3g}")
 
 
@@ -182,6 +212,32 @@ def test_pipeline_with_dense_first_layers():
     case = make_case(seed=5, L=3)
     outs, _ = run_gpu(case, dense_layers=(0,))
     check_against_oracle(case, outs, dense_layers=(0,))
+
+
+@pytest.mark.parametrize("select_x", [0, 1])
+def test_pipeline_with_drafts(select_x):
+    """Draft lookahead: layers 0 and 2 run their draft group at step 1 and
+    select the next block with the draft KV as normalisation tail (layer 1
+    has no draft); every denoising output, every draft-group output and so
+    every pool matches the oracle's schedule with drafts."""
+    case = make_case(seed=7, L=3, T=3, drafts=True)
+    outs, _ = run_gpu(case, draft_layers=(0, 2), select_x=select_x)
+    check_against_oracle(case, outs, draft_layers=(0, 2), select_x=select_x)
+
+
+def test_pipeline_with_drafts_and_a_dense_layer_bitwise_single_stream():
+    case = make_case(seed=8, L=2, T=2, drafts=True)
+    ref, _ = run_gpu(case, one_stream=True, draft_layers=(0, 1), dense_layers=(0,))
+    got, _ = run_gpu(case, delay_main=1_000_000, draft_layers=(0, 1), dense_layers=(0,))
+    for n in range(case["nblocks"]):
+        for l in range(case["L"] + 1):
+            a, b = got[n][l], ref[n][l]
+            if isinstance(a, list):
+                for x, y in zip(a, b):
+                    assert x.tobytes() == y.tobytes(), (n, l)
+            else:
+                assert a.tobytes() == b.tobytes(), (n, l)
+    check_against_oracle(case, got, dense_layers=(0,), draft_layers=(0, 1))
 
 
 def test_pipeline_layer32k_shapes_one_block():

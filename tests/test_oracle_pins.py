@@ -546,12 +546,26 @@ def test_full_budget_schedule_with_drafts_is_dense_decoding(x):
             v_done=_rand(rng, (B, Hkv, d), "f64"),
             k_draft=_rand(rng, (B, Hkv, d), "f64") * 4.0,
             q_next=_rand(rng, (B, Hq, d), "f64")))
+    for blk in blocks:
+        blk["q_draft"] = _rand(rng, (B, Hq, d), "f64")
+        blk["v_draft"] = _rand(rng, (B, Hkv, d), "f64")
     idx0 = np.tile(np.arange(S0, dtype=np.int32), (Hkv, 1))
-    with_d = oracle.decode_blocks(K0, V0, idx0, blocks, num=1, den=1, x=x)
+    douts = []
+    with_d = oracle.decode_blocks(K0, V0, idx0, blocks, num=1, den=1, x=x, draft_outs=douts)
     without = oracle.decode_blocks(K0, V0, idx0, [{k: v for k, v in b.items() if k != "k_draft"}
                                                   for b in blocks], num=1, den=1)
     for a, b in zip(with_d, without):
         np.testing.assert_array_equal(a, b)
+    # the draft group: dense attention over the prefix before its block plus
+    # the draft's own KV (at 100% the pool is the whole prefix)
+    Kc, Vc = K0, V0
+    for n, blk in enumerate(blocks):
+        keys = np.concatenate([Kc, blk["k_draft"].transpose(1, 0, 2)], axis=1)
+        vals = np.concatenate([Vc, blk["v_draft"].transpose(1, 0, 2)], axis=1)
+        np.testing.assert_allclose(douts[n], _sdpa(blk["q_draft"], keys, vals),
+                                   rtol=1e-12, atol=1e-13)
+        Kc = np.concatenate([Kc, blk["k_done"].transpose(1, 0, 2)], axis=1)
+        Vc = np.concatenate([Vc, blk["v_done"].transpose(1, 0, 2)], axis=1)
 
 
 def test_schedule_with_draft_selects_with_the_draft_as_tail():
