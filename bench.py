@@ -45,6 +45,12 @@ def parse():
                     help="timed blocks of the 36-layer pipeline workload")
     ap.add_argument("--dense-layers", type=int, default=0,
                     help="36-layer workload: how many first layers keep exact attention")
+    ap.add_argument("--drafts", action="store_true",
+                    help="36-layer workload: draft lookahead (draft group at step 1, the next "
+                         "selection after it with the draft KV as normalisation tail)")
+    ap.add_argument("--select-x", type=int, default=0, choices=[0, 1],
+                    help="36-layer workload: next-block representative query, 0 the mean of "
+                         "the block's queries, 1 its centre row")
     ap.add_argument("--dense", action="store_true",
                     help="denoise over the full cache (GPU-only dense baseline)")
     ap.add_argument("--reps", type=int, default=30, help="isolated kernel timing reps")
@@ -533,6 +539,12 @@ def bench_pipeline36(args):
             dvv=synth.device_normal(wl, gen, (b, B, Hkv, d), dev),
             qn=synth.device_queries(wl, u, gen, (), dev),
             out=torch.empty((b, B, Hq, d), dtype=torch.bfloat16, device=dev)))
+        if args.drafts:
+            layers[-1].update(
+                qd=synth.device_queries(wl, u, gen, (), dev),
+                ddk=synth.device_normal(wl, gen, (b, B, Hkv, d), dev),
+                ddv=synth.device_normal(wl, gen, (b, B, Hkv, d), dev),
+                od=torch.empty((b, B, Hq, d), dtype=torch.bfloat16, device=dev))
     torch.cuda.synchronize()
     s_main = torch.cuda.Stream(device=dev)
     s_retr = torch.cuda.Stream(device=dev)
@@ -563,6 +575,11 @@ def bench_pipeline36(args):
                            Ly["bk"].data_ptr(), Ly["bv"].data_ptr(), Ly["dk"].data_ptr(),
                            Ly["dvv"].data_ptr(), Ly["qn"].data_ptr(), Ly["out"].data_ptr(), 0,
                            int(l < nd)) for l, Ly in enumerate(layers)]
+            for Lr, Ly in zip(lay, layers):
+                Lr.select_x = args.select_x
+                if args.drafts:
+                    Lr.q_draft, Lr.draft_k = Ly["qd"].data_ptr(), Ly["ddk"].data_ptr()
+                    Lr.draft_v, Lr.out_draft = Ly["ddv"].data_ptr(), Ly["od"].data_ptr()
             torch.cuda.synchronize()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
@@ -589,6 +606,7 @@ def bench_pipeline36(args):
            "data": "synthetic, generated on the device (seeded torch generator)",
            "config": {"workload": wl.name, "layers": L, "batch": b, "seq_len": S0, "block": B,
                       "steps": T, "budget": "5%", "dense_layers": nd,
+                      "drafts": bool(args.drafts), "select_x": args.select_x,
                       "step": "one block: next-block selection of "
                       "all layers on the retrieval stream, T x L denoising steps on the main "
                       "stream, join, append, swap"},
