@@ -87,7 +87,7 @@ def _load():
                                             i64, p, p]
     lib.herald_oracle_select_draft.restype = i32
     lib.herald_oracle_select_draft.argtypes = [i32, i32, i32, i32, i32, i64, p, i32, p, i32,
-                                               p, i32, i64, i64, p, p]
+                                               p, i32, i64, i64, p, p, p, p, p]
     lib.herald_oracle_gather.restype = i32
     lib.herald_oracle_gather.argtypes = [i32, i32, i64, p, i32, p, i64, i64, p]
     lib.herald_oracle_attn.restype = i32
@@ -173,9 +173,11 @@ def select_xq(q_sel, K, k: int, x: int):
     return idx, s_hat
 
 
-def select_draft(q_sel, K, tail, k: int, x: int = 0):
+def select_draft(q_sel, K, tail, k: int, x: int = 0, V=None, tail_v=None):
     """One sequence. q_sel [B][Hq][d], K [Hkv][S][d], tail [n][Hkv][d] (or
-    None). Returns (idx int32 [Hkv][k] ascending, s_hat float64 [Hkv][S])."""
+    None). Returns (idx int32 [Hkv][k] ascending, s_hat float64 [Hkv][S]);
+    with V [Hkv][S][d] (and tail_v like tail) also the attention output of
+    every representative row, float64 [max(x,1)][Hq][d]."""
     q, qt = _as_np(q_sel)
     kk, kt = _as_np(K)
     B, Hq, d = q.shape
@@ -189,12 +191,24 @@ def select_draft(q_sel, K, tail, k: int, x: int = 0):
         n = tt.shape[0]
     idx = np.empty((Hkv, k), np.int32)
     s_hat = np.empty((Hkv, S), np.float64)
+    o = vv = tv = None
+    if V is not None:
+        vv, vt = _as_np(V)
+        assert vt == kt and vv.shape == kk.shape
+        if tail_v is not None:
+            tv, tvt = _as_np(tail_v)
+            assert tvt == ttype and tv.shape == tt.shape
+        elif n:
+            raise ValueError("tail_v is needed with a tail")
+        o = np.empty((max(int(x), 1), Hq, d), np.float64)
     rc = _load().herald_oracle_select_draft(B, int(x), Hq, Hkv, d, S, _ptr(q), qt, _ptr(kk),
                                             kt, _ptr(tt), ttype, n, int(k), _ptr(s_hat),
-                                            _ptr(idx))
+                                            _ptr(idx), None if vv is None else _ptr(vv),
+                                            None if tv is None else _ptr(tv),
+                                            None if o is None else _ptr(o))
     if rc != 0:
         raise ValueError("herald_oracle_select_draft: bad arguments")
-    return idx, s_hat
+    return (idx, s_hat) if o is None else (idx, s_hat, o)
 
 
 def attn_groups(q, ctx_k, ctx_v, blk_k, blk_v, groups: int):

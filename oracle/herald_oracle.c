@@ -42,7 +42,11 @@
  *                          statistics (m, l) but the draft rows are never
  *                          candidates, since the completed block replaces
  *                          them (a reading: the paper appends the draft to
- *                          the pool it ranks).
+ *                          the pool it ranks). Optionally also the attention
+ *                          output of every score row over cache and draft,
+ *                          o = sum_s exp(z[s]-m)/l v_s (the running output o_g
+ *                          that the paper's fused selection kernel keeps,
+ *                          sec. IV-B.4).
  *   herald_oracle_gather   copy of the selected K/V rows into a dense pool
  *                          (sec. IV-B.3, the gather of the selected entries).
  *   herald_oracle_attn     B-query GQA attention of a block over a context
@@ -255,15 +259,19 @@ int herald_oracle_select_xq(int B, int x, int Hq, int Hkv, int d, int64_t S,
  * tail [n_tail][Hkv][d] (row t of head h at (t*Hkv + h)*d), n_tail >= 0.
  * x = 0: one score row per query head, the mean of the B queries; x >= 1:
  * the x centred rows as herald_oracle_select_xq. Writes s_hat [Hkv][S] (if
- * non-NULL) and idx [Hkv][k] (ascending), candidates 0 .. S-1 only.
+ * non-NULL) and idx [Hkv][k] (ascending), candidates 0 .. S-1 only. With
+ * o_out: Vc [Hkv][S][d] (type k_type) and tail_v (type t_type, like tail)
+ * give the values, and o_out [max(x,1)][Hq][d] the attention outputs.
  */
 int herald_oracle_select_draft(int B, int x, int Hq, int Hkv, int d, int64_t S,
                                const void *q_sel, int q_type, const void *K,
                                int k_type, const void *tail, int t_type,
                                int64_t n_tail, int64_t k, double *s_hat_out,
-                               int32_t *idx_out) {
+                               int32_t *idx_out, const void *Vc, const void *tail_v,
+                               double *o_out) {
   if (B < 1 || x < 0 || x > B || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 ||
-      S < 1 || k < 1 || k > S || n_tail < 0 || (n_tail > 0 && !tail))
+      S < 1 || k < 1 || k > S || n_tail < 0 || (n_tail > 0 && !tail) ||
+      (o_out && (!Vc || (n_tail > 0 && !tail_v))))
     return -1;
   const int G = Hq / Hkv;
   const int nrow = x == 0 ? 1 : x;   /* query rows per head */
@@ -329,6 +337,19 @@ int herald_oracle_select_draft(int B, int x, int Hq, int Hkv, int d, int64_t S,
       r[s].idx = s;
       if (s_hat_out) s_hat_out[(int64_t)h * S + s] = acc;
     }
+    /* attention output of every score row over prefix and tail, written at
+     * [v / G][h * G + v % G][e] of o_out [nrow][Hq][d] */
+    if (o_out)
+      for (int v = 0; v < V; ++v)
+        for (int e = 0; e < d; ++e) {
+          double acc = 0.0;
+          for (int64_t s = 0; s < N; ++s) {
+            const double vv = s < S ? load_elem(Vc, k_type, ((int64_t)h * S + s) * d + e)
+                                    : load_elem(tail_v, t_type, ((s - S) * Hkv + h) * d + e);
+            acc += exp(z[(int64_t)v * N + s] - m[v]) / l[v] * vv;
+          }
+          o_out[((int64_t)(v / G) * Hq + h * G + v % G) * d + e] = acc;
+        }
     topk_ascending(r, S, k, idx_out + (int64_t)h * k);
     free(qv); free(z); free(m); free(l); free(r);
   }

@@ -596,3 +596,27 @@ def test_schedule_with_draft_selects_with_the_draft_as_tail():
                  np.concatenate([pool_k, blocks[1]["k_steps"][0].transpose(1, 0, 2)], 1),
                  np.concatenate([pool_v, blocks[1]["v_steps"][0].transpose(1, 0, 2)], 1))
     np.testing.assert_allclose(outs[1][0], want, rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("x,n", [(0, 0), (0, 3), (1, 3), (3, 2)])
+def test_selection_output_is_sdpa_of_the_representative_rows(x, n):
+    """The attention output kept beside the ranking is exact attention of
+    each representative row over the cache plus the draft (fp64 SDPA)."""
+    rng = np.random.default_rng(200 + 10 * x + n)
+    B, Hq, Hkv, d, S = 5, 8, 2, 16, 120
+    q_sel = _rand(rng, (B, Hq, d), "f64")
+    K, V = _rand(rng, (Hkv, S, d), "f64"), _rand(rng, (Hkv, S, d), "f64")
+    tk = _rand(rng, (n, Hkv, d), "f64") if n else None
+    tv = _rand(rng, (n, Hkv, d), "f64") if n else None
+    idx, s, o = oracle.select_draft(q_sel, K, tk, 9, x, V=V, tail_v=tv)
+    idx0, s0 = oracle.select_draft(q_sel, K, tk, 9, x)
+    np.testing.assert_array_equal(idx, idx0)
+    np.testing.assert_array_equal(s, s0)
+    keys = K if not n else np.concatenate([K, tk.transpose(1, 0, 2)], axis=1)
+    vals = V if not n else np.concatenate([V, tv.transpose(1, 0, 2)], axis=1)
+    if x == 0:
+        rows = q_sel.mean(0, keepdims=True)
+    else:
+        c0 = (B - x) // 2
+        rows = q_sel[c0:c0 + x]
+    np.testing.assert_allclose(o, _sdpa(rows, keys, vals), rtol=1e-12, atol=1e-13)
