@@ -19,7 +19,9 @@
  *                      sec. IV-A.2).
  *   herald_select_draft the next block's selection with the current
  *                      block's draft KV appended for normalisation
- *                      (draft-based lookahead, sec. IV-A.1, sec. IV-B.2).
+ *                      (draft-based lookahead, sec. IV-A.1, sec. IV-B.2);
+ *                      herald_select_attn also returns the representative
+ *                      queries' attention output (sec. IV-B.4).
  *   herald_gather      copies the selected K/V rows into a sparse pool
  *                      (sec. IV-B.3).
  *   herald_block_attn  B-query GQA attention over a context (a pool, or a
@@ -201,6 +203,29 @@ herald_status herald_select_draft(const herald_heads *heads, int32_t batch,
                                   int32_t n_draft, const int32_t *k_per_seq,
                                   int32_t k_max, int32_t *idx_out, void *ws,
                                   size_t ws_bytes, hipStream_t stream);
+
+/*
+ * herald_select_draft plus the attention output of the representative
+ * queries over the cache and the draft: for every score row (representative
+ * row i, query head hq = h * G + g), o = sum_s exp(z[s] - m) / l * v_s over
+ * the kv->seq_lens[b] cached rows and the n_draft draft rows, with the same
+ * fp64 scores and statistics as the ranking (the running output o_g that the
+ * paper's fused selection kernel keeps beside (m, l) and hands to the FFN,
+ * sec. IV-B.4). Weights in fp32, fp32 accumulation, then heads->dtype (bf16
+ * rounded to nearest-even).
+ *   kv        K and V are read.
+ *   draft_v   device [batch][n_draft][H_kv][d] (the draft's V); may be NULL
+ *             if n_draft = 0.
+ *   o_out     device [batch][max(x, 1)][H_q][d], 16-byte aligned (not NULL).
+ * Other arguments and the workspace as herald_select_draft.
+ */
+herald_status herald_select_attn(const herald_heads *heads, int32_t batch,
+                                 int32_t block, int32_t x, const void *q_sel,
+                                 const herald_kv *kv, const void *draft_k,
+                                 const void *draft_v, int32_t n_draft,
+                                 const int32_t *k_per_seq, int32_t k_max,
+                                 int32_t *idx_out, void *o_out, void *ws,
+                                 size_t ws_bytes, hipStream_t stream);
 
 /*
  * Gather (sec. IV-B.3): for each (b, h) and j < k_b, copies row idx[b][h][j]

@@ -143,9 +143,9 @@ size_t herald_select_workspace(const herald_heads *heads, int32_t batch, int64_t
 // softmax statistics only.
 static herald_status select_common(const herald_heads *heads, int32_t batch, int32_t block,
                                    int32_t x, const void *q_sel, const herald_kv *kv,
-                                   const void *tail, int32_t n_tail, const int32_t *k_per_seq,
-                                   int32_t k_max, int32_t *idx_out, void *ws, size_t ws_bytes,
-                                   hipStream_t stream) {
+                                   const void *tail, const void *tail_v, int32_t n_tail,
+                                   const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
+                                   void *o_out, void *ws, size_t ws_bytes, hipStream_t stream) {
   herald_status st;
   if ((st = check_heads(heads)) != HERALD_OK) return st;
   if ((st = check_block(block)) != HERALD_OK) return st;
@@ -153,10 +153,12 @@ static herald_status select_common(const herald_heads *heads, int32_t batch, int
     return HERALD_ERR_INVALID_ARG;
   if (n_tail < 0 || n_tail > 64 || (n_tail > 0 && (!tail || !aligned16(tail))))
     return HERALD_ERR_INVALID_ARG;
+  if (o_out && (!aligned16(o_out) || (n_tail > 0 && (!tail_v || !aligned16(tail_v)))))
+    return HERALD_ERR_INVALID_ARG;
   const int G = heads->num_q_heads / heads->num_kv_heads;
   const int V = (x == 0 ? 1 : x) * G;
   if (V > kMaxScoreRows) return HERALD_ERR_UNSUPPORTED;
-  if ((st = check_kv(heads, kv, false)) != HERALD_OK) return st;
+  if ((st = check_kv(heads, kv, o_out != nullptr)) != HERALD_OK) return st;  // V for o_out
   if (k_max < 1 || k_max > kv->max_seq_len) return HERALD_ERR_INVALID_ARG;
   const size_t need = herald_select_xq_workspace(heads, batch, x == 0 ? 1 : x, kv->max_seq_len);
   if (!ws || !aligned256(ws) || ws_bytes < need) return HERALD_ERR_WORKSPACE;
@@ -164,18 +166,18 @@ static herald_status select_common(const herald_heads *heads, int32_t batch, int
   select_ws_bytes(batch, V * heads->num_kv_heads, heads->num_kv_heads, heads->head_dim,
                   kv->max_seq_len, &layout, reinterpret_cast<char *>(ws));
   if (x == 0)
-    return hip_status(launch_select(*heads, batch, block, q_sel, view_of(kv), tail, n_tail,
-                                    k_per_seq, k_max, idx_out, layout, stream));
-  return hip_status(launch_select_xq(*heads, batch, block, x, q_sel, view_of(kv), tail, n_tail,
-                                     k_per_seq, k_max, idx_out, layout, stream));
+    return hip_status(launch_select(*heads, batch, block, q_sel, view_of(kv), tail, tail_v,
+                                    n_tail, k_per_seq, k_max, idx_out, o_out, layout, stream));
+  return hip_status(launch_select_xq(*heads, batch, block, x, q_sel, view_of(kv), tail, tail_v,
+                                     n_tail, k_per_seq, k_max, idx_out, o_out, layout, stream));
 }
 
 herald_status herald_select(const herald_heads *heads, int32_t batch, int32_t block,
                             const void *q_sel, const herald_kv *kv,
                             const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
                             void *ws, size_t ws_bytes, hipStream_t stream) {
-  return select_common(heads, batch, block, 0, q_sel, kv, nullptr, 0, k_per_seq, k_max,
-                       idx_out, ws, ws_bytes, stream);
+  return select_common(heads, batch, block, 0, q_sel, kv, nullptr, nullptr, 0, k_per_seq,
+                       k_max, idx_out, nullptr, ws, ws_bytes, stream);
 }
 
 size_t herald_select_xq_workspace(const herald_heads *heads, int32_t batch, int32_t x,
@@ -193,8 +195,8 @@ herald_status herald_select_xq(const herald_heads *heads, int32_t batch, int32_t
                                const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
                                void *ws, size_t ws_bytes, hipStream_t stream) {
   if (x < 1) return HERALD_ERR_INVALID_ARG;
-  return select_common(heads, batch, block, x, q_sel, kv, nullptr, 0, k_per_seq, k_max,
-                       idx_out, ws, ws_bytes, stream);
+  return select_common(heads, batch, block, x, q_sel, kv, nullptr, nullptr, 0, k_per_seq,
+                       k_max, idx_out, nullptr, ws, ws_bytes, stream);
 }
 
 herald_status herald_select_draft(const herald_heads *heads, int32_t batch, int32_t block,
@@ -202,8 +204,18 @@ herald_status herald_select_draft(const herald_heads *heads, int32_t batch, int3
                                   const void *draft_k, int32_t n_draft,
                                   const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
                                   void *ws, size_t ws_bytes, hipStream_t stream) {
-  return select_common(heads, batch, block, x, q_sel, kv, draft_k, n_draft, k_per_seq, k_max,
-                       idx_out, ws, ws_bytes, stream);
+  return select_common(heads, batch, block, x, q_sel, kv, draft_k, nullptr, n_draft, k_per_seq,
+                       k_max, idx_out, nullptr, ws, ws_bytes, stream);
+}
+
+herald_status herald_select_attn(const herald_heads *heads, int32_t batch, int32_t block,
+                                 int32_t x, const void *q_sel, const herald_kv *kv,
+                                 const void *draft_k, const void *draft_v, int32_t n_draft,
+                                 const int32_t *k_per_seq, int32_t k_max, int32_t *idx_out,
+                                 void *o_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!o_out) return HERALD_ERR_INVALID_ARG;
+  return select_common(heads, batch, block, x, q_sel, kv, draft_k, draft_v, n_draft, k_per_seq,
+                       k_max, idx_out, o_out, ws, ws_bytes, stream);
 }
 
 herald_status herald_gather(const herald_heads *heads, int32_t batch, const herald_kv *kv,
@@ -359,10 +371,10 @@ herald_status herald_decode_block(const herald_heads *heads, int32_t num_layers,
       const void *tail = L.q_draft ? L.draft_k : nullptr;
       const int n_tail = L.q_draft ? block : 0;
       r = L.select_x == 0
-              ? launch_select(*heads, batch, block, L.q_next, view_of(&cache), tail, n_tail,
-                              k_next, k_max, idx, sel, s_retr)
+              ? launch_select(*heads, batch, block, L.q_next, view_of(&cache), tail, nullptr,
+                              n_tail, k_next, k_max, idx, nullptr, sel, s_retr)
               : launch_select_xq(*heads, batch, block, 1, L.q_next, view_of(&cache), tail,
-                                 n_tail, k_next, k_max, idx, sel, s_retr);
+                                 nullptr, n_tail, k_next, k_max, idx, nullptr, sel, s_retr);
       if (r == hipSuccess)
         r = launch_gather(*heads, batch, view_of(&cache), idx, k_next, k_max, pool_of(&L.idle),
                           0, s_retr);

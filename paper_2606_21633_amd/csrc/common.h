@@ -92,6 +92,7 @@ struct SelectWs {
                     // of the normalisation tail
   uint64_t *keys;   // [b][Hkv][S_pad]
   uint32_t *hist;   // [b][Hkv][2048]
+  float *opart;     // [b][Hkv][nchunk + 1][G][d]: attention output parts (optional output)
   int64_t S_pad;
   int nchunk;
 };
@@ -111,16 +112,20 @@ constexpr int kMaxScoreRows = 512;
 // rows that enter every score row's (max, sum exp) but are never ranked
 // (n_tail = 0: none).
 hipError_t launch_select_xq(const herald_heads &hd, int batch, int block, int x,
-                            const void *q_sel, const KvView &kv, const void *tail, int n_tail,
-                            const int32_t *k_per_seq, int k_max, int32_t *idx_out,
-                            const SelectWs &ws, hipStream_t stream);
+                            const void *q_sel, const KvView &kv, const void *tail,
+                            const void *tail_v, int n_tail, const int32_t *k_per_seq, int k_max,
+                            int32_t *idx_out, void *o_out, const SelectWs &ws,
+                            hipStream_t stream);
 
 // Selection with the mean of the block's queries as the representative;
 // tail as above.
+// tail_v and o_out: the optional attention output of every score row over
+// the cache and the tail, [b][V / G][Hq][d] (o_out null: none).
 hipError_t launch_select(const herald_heads &hd, int batch, int block,
-                         const void *q_sel, const KvView &kv, const void *tail, int n_tail,
-                         const int32_t *k_per_seq, int k_max, int32_t *idx_out,
-                         const SelectWs &ws, hipStream_t stream);
+                         const void *q_sel, const KvView &kv, const void *tail,
+                         const void *tail_v, int n_tail, const int32_t *k_per_seq, int k_max,
+                         int32_t *idx_out, void *o_out, const SelectWs &ws,
+                         hipStream_t stream);
 
 hipError_t launch_gather(const herald_heads &hd, int batch, const KvView &kv,
                          const int32_t *idx, const int32_t *k_per_seq, int k_max,

@@ -47,6 +47,30 @@ __device__ __forceinline__ void merge_ml(double &m, double &l, double m2, double
   else { l += l2 * exp(m2 - m); }
 }
 
+// (m, 1 / l) of score row v of (b, h) over the whole cache and the tail:
+// the nch chunk partials, then the tail slot, merged by one wave in a fixed
+// order (lower lane first), so that every caller, in every lane, gets
+// bit-identical values.
+__device__ __forceinline__ void merged_stats(const double *__restrict__ part, int64_t bh,
+                                             int nslot, int nch, int V, int v, int lane,
+                                             double &m_out, double &inv_out) {
+  double m = -INFINITY, l = 0.0;
+  for (int c = lane; c <= nch; c += 64) {
+    const int slot = c < nch ? c : nslot - 1;  // the chunks, then the tail
+    const double *p = part + ((bh * nslot + slot) * V + v) * 2;
+    merge_ml(m, l, p[0], p[1]);
+  }
+#pragma unroll
+  for (int off = 1; off <= 32; off <<= 1) {
+    const double m2 = __shfl_xor(m, off, 64);
+    const double l2 = __shfl_xor(l, off, 64);
+    if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
+    else merge_ml(m, l, m2, l2);
+  }
+  m_out = m;
+  inv_out = 1.0 / l;
+}
+
 // ---------------------------------------------------------------- repq
 template <int D, int G, bool BF16>
 __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_sel,
@@ -463,21 +487,9 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
   // Every workgroup of this (b, h) merges the same partials in the same
   // order, so all of them see bit-identical (m_g, l_g).
   for (int g = wave; g < G; g += 4) {
-    double m = -INFINITY, l = 0.0;
-    for (int c = lane; c <= nch; c += 64) {
-      const int slot = c < nch ? c : nslot - 1;  // the chunks, then the tail
-      const double *p = part + ((bh * nslot + slot) * G + g) * 2;
-      merge_ml(m, l, p[0], p[1]);
-    }
-#pragma unroll
-    for (int off = 1; off <= 32; off <<= 1) {
-      const double m2 = __shfl_xor(m, off, 64);
-      const double l2 = __shfl_xor(l, off, 64);
-      // merge in a fixed (lower lane first) order
-      if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
-      else merge_ml(m, l, m2, l2);
-    }
-    if (lane == 0) { sm[g] = m; sinv[g] = 1.0 / l; }
+    double m, inv;
+    merged_stats(part, bh, nslot, nch, G, g, lane, m, inv);
+    if (lane == 0) { sm[g] = m; sinv[g] = inv; }
   }
   __syncthreads();
   double m[G], inv[G];
@@ -747,20 +759,9 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
 
   // every workgroup of this (b, h) merges the same partials in the same order
   for (int v = wave; v < V; v += 4) {
-    double m = -INFINITY, l = 0.0;
-    for (int c = lane; c <= nch; c += 64) {
-      const int slot = c < nch ? c : nslot - 1;  // the chunks, then the tail
-      const double *p = part + ((bh * nslot + slot) * V + v) * 2;
-      merge_ml(m, l, p[0], p[1]);
-    }
-#pragma unroll
-    for (int off = 1; off <= 32; off <<= 1) {
-      const double m2 = __shfl_xor(m, off, 64);
-      const double l2 = __shfl_xor(l, off, 64);
-      if (lane & off) { double tm = m2, tl = l2; merge_ml(tm, tl, m, l); m = tm; l = tl; }
-      else merge_ml(m, l, m2, l2);
-    }
-    if (lane == 0) { sm[v] = m; sinv[v] = 1.0 / l; }
+    double m, inv;
+    merged_stats(part, bh, nslot, nch, V, v, lane, m, inv);
+    if (lane == 0) { sm[v] = m; sinv[v] = inv; }
   }
   __syncthreads();
 
@@ -797,6 +798,159 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
   __syncthreads();
   for (int t = threadIdx.x; t < kHistBins; t += 256)
     if (sh_hist[t]) atomicAdd(&hist[bh * kHistBins + t], sh_hist[t]);
+}
+
+// ---------------------------------------------------------------- attention output
+// Optional output of the selection: the attention of every score row v over
+// the cache and the tail, o_v = sum_s exp(z_v[s] - m_v) / l_v * v_s (the
+// output accumulator that the paper's fused kernel keeps beside (m, l),
+// sec. IV-B.4), from the spilled fp64 scores and the merged statistics, with
+// fp32 weights and fp32 accumulation. out_kernel: one workgroup per (chunk,
+// KV head, sequence) writes the chunk's partial sum [V][D]; thread t takes
+// elements 2 (t % (D/2)) + {0, 1} of score rows t / (D/2) + VS j (VS = 512 / D
+// slots, NV rows per slot and pass); the weights of 32 cached rows at a time
+// are formed once in LDS and read by every thread of a wave at one address.
+template <int D, int NV, bool BF16>
+__global__ __launch_bounds__(256) void out_kernel(KvView kv, const double *__restrict__ zspill,
+                                                  const double *__restrict__ part,
+                                                  float *__restrict__ opart, int Hkv, int V,
+                                                  int64_t S_pad, int nslot) {
+  constexpr int ELT = BF16 ? 2 : 4;
+  constexpr int EP = D / 2;       // element pairs of a row
+  constexpr int VS = 256 / EP;    // score-row slots
+  constexpr int VB = VS * NV;     // score rows per pass
+  constexpr int TR = 32;          // cached rows per weight tile
+  __shared__ double sm[kMaxScoreRows], sinv[kMaxScoreRows];
+  __shared__ float wt[TR][VB];
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t S = kv_len(kv, b);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S) return;
+  const int nch = (int)((S + kScoreChunk - 1) / kScoreChunk);
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int v = wave; v < V; v += 4) {
+    double m, inv;
+    merged_stats(part, bh, nslot, nch, V, v, lane, m, inv);
+    if (lane == 0) { sm[v] = m; sinv[v] = inv; }
+  }
+  __syncthreads();
+  const int ep = threadIdx.x % EP, vs = threadIdx.x / EP;
+  const int64_t c1 = min(c0 + (int64_t)kScoreChunk, S);
+  for (int vb0 = 0; vb0 < V; vb0 += VB) {
+    float acc[NV][2];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) acc[j][0] = acc[j][1] = 0.f;
+    for (int64_t r0 = c0; r0 < c1; r0 += TR) {
+      for (int i = threadIdx.x; i < TR * VB; i += 256) {
+        const int rr = i / VB, v = vb0 + i % VB;
+        const int64_t s = r0 + rr;
+        float w = 0.f;
+        if (s < c1 && v < V)
+          w = (float)(exp(zspill[(bh * S_pad + s) * V + v] - sm[v]) * sinv[v]);
+        wt[rr][i % VB] = w;
+      }
+      __syncthreads();
+      const int nr = (int)min((int64_t)TR, c1 - r0);
+      for (int rr = 0; rr < nr; ++rr) {
+        const char *row = kv.v + kv_row(kv, b, h, r0 + rr) * ELT;
+        float x0, x1;
+        if (BF16) {
+          const uint32_t w2 = *reinterpret_cast<const uint32_t *>(row + 4 * ep);
+          x0 = bf16_lo(w2);
+          x1 = bf16_hi(w2);
+        } else {
+          const float2 f2 = *reinterpret_cast<const float2 *>(row + 8 * ep);
+          x0 = f2.x;
+          x1 = f2.y;
+        }
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+          const float w = wt[rr][vs + VS * j];
+          acc[j][0] = fmaf(w, x0, acc[j][0]);
+          acc[j][1] = fmaf(w, x1, acc[j][1]);
+        }
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int v = vb0 + vs + VS * j;
+      if (v < V) {
+        float *o = opart + ((bh * nslot + chunk) * V + v) * D + 2 * ep;
+        o[0] = acc[j][0];
+        o[1] = acc[j][1];
+      }
+    }
+  }
+}
+
+// The tail rows' part of the attention output, into the last partial slot:
+// one wave per score row; the lanes first form the tail scores (as
+// tail_kernel does) and weights, then sum weight x V over the tail rows for
+// two elements each.
+template <bool BF16>
+__global__ __launch_bounds__(256) void out_tail_kernel(const double *__restrict__ qbar,
+                                                       const void *__restrict__ tail_k,
+                                                       const void *__restrict__ tail_v,
+                                                       int n_tail, const int32_t *lens,
+                                                       int64_t max_len,
+                                                       const double *__restrict__ part,
+                                                       float *__restrict__ opart, int Hkv, int V,
+                                                       int D, int nslot, double scale) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int nch = (int)((S + kScoreChunk - 1) / kScoreChunk);
+  auto elem = [&](const void *p, int64_t i) -> double {
+    return BF16 ? (double)bf16_lo(reinterpret_cast<const uint16_t *>(p)[i])
+                : (double)reinterpret_cast<const float *>(p)[i];
+  };
+  for (int v = wave; v < V; v += 4) {
+    double m, inv;
+    merged_stats(part, bh, nslot, nch, V, v, lane, m, inv);
+    float w = 0.f;
+    if (lane < n_tail) {
+      const int64_t row = (((int64_t)b * n_tail + lane) * Hkv + h) * D;
+      double acc = 0.0;
+      for (int e = 0; e < D; ++e) acc = fma(qbar[(bh * D + e) * V + v], elem(tail_k, row + e), acc);
+      w = (float)(exp(acc * scale - m) * inv);
+    }
+    for (int e = lane; e < D; e += 64) {
+      float o = 0.f;
+      for (int t = 0; t < n_tail; ++t) {
+        const float wt = __shfl(w, t, 64);
+        o = fmaf(wt, (float)elem(tail_v, (((int64_t)b * n_tail + t) * Hkv + h) * D + e), o);
+      }
+      opart[((bh * nslot + nslot - 1) * V + v) * D + e] = o;
+    }
+  }
+}
+
+// o[b][i][h G + g][e] (v = i G + g) = the chunks' parts in chunk order, then
+// the tail's; bf16 outputs rounded to nearest-even.
+template <bool BF16>
+__global__ __launch_bounds__(256) void out_combine_kernel(const int32_t *lens, int64_t max_len,
+                                                          const float *__restrict__ opart,
+                                                          void *__restrict__ o_out, int n_tail,
+                                                          int Hq, int Hkv, int V, int D,
+                                                          int nslot) {
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= V * D) return;
+  const int v = t / D, e = t % D, G = Hq / Hkv, i = v / G, g = v % G;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int nch = (int)((S + kScoreChunk - 1) / kScoreChunk);
+  float acc = 0.f;
+  for (int c = 0; c < nch; ++c) acc += opart[((bh * nslot + c) * V + v) * D + e];
+  if (n_tail > 0) acc += opart[((bh * nslot + nslot - 1) * V + v) * D + e];
+  const int64_t dst = (((int64_t)b * (V / G) + i) * Hq + h * G + g) * D + e;
+  if (BF16)
+    reinterpret_cast<uint16_t *>(o_out)[dst] = (uint16_t)f32_to_bf16_rne(acc);
+  else
+    reinterpret_cast<float *>(o_out)[dst] = acc;
 }
 
 // ---------------------------------------------------------------- topk
@@ -1014,11 +1168,36 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   for (int j = k + tid; j < k_max; j += kTopkThreads) out[j] = -1;
 }
 
+// The optional attention output (after norm has written the keys: the
+// statistics are in place), o_out [b][V / G][Hq][D].
+template <int D, bool BF16>
+void launch_out(const KvView &kv, int batch, int Hq, int Hkv, int V, const void *tail,
+                const void *tail_v, int n_tail, void *o_out, const SelectWs &ws, int nslot,
+                double scale, hipStream_t stream) {
+  const dim3 grid(ws.nchunk, Hkv, batch);
+  constexpr int VS = 512 / D;  // score-row slots of out_kernel
+  if (V <= VS)
+    out_kernel<D, 1, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
+                                                     ws.S_pad, nslot);
+  else if (V <= 4 * VS)
+    out_kernel<D, 4, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
+                                                     ws.S_pad, nslot);
+  else
+    out_kernel<D, 16, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
+                                                      ws.S_pad, nslot);
+  if (n_tail > 0)
+    out_tail_kernel<BF16><<<dim3(Hkv, batch), 256, 0, stream>>>(
+        ws.qbar, tail, tail_v, n_tail, kv.lens, kv.max_len, ws.part, ws.opart, Hkv, V, D, nslot,
+        scale);
+  out_combine_kernel<BF16><<<dim3((V * D + 255) / 256, Hkv, batch), 256, 0, stream>>>(
+      kv.lens, kv.max_len, ws.opart, o_out, n_tail, Hq, Hkv, V, D, nslot);
+}
+
 template <int D, int G, bool BF16>
 hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView &kv,
-                           int Hq, int Hkv, const void *tail, int n_tail,
+                           int Hq, int Hkv, const void *tail, const void *tail_v, int n_tail,
                            const int32_t *k_per_seq, int k_max, int32_t *idx_out,
-                           const SelectWs &ws, hipStream_t stream) {
+                           void *o_out, const SelectWs &ws, hipStream_t stream) {
   const double scale = 1.0 / sqrt((double)D);
   const int nslot = ws.nchunk + 1;  // partial slots per (b, h): chunks, then the tail
   repq_kernel<D, G, BF16><<<dim3(Hkv, batch, (D * G + 255) / 256), 256, 0, stream>>>(
@@ -1046,6 +1225,9 @@ hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView
                                            Hkv, ws.S_pad, nslot, kv.max_len);
   topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
       kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
+  if (o_out)
+    launch_out<D, BF16>(kv, batch, Hq, Hkv, G, tail, tail_v, n_tail, o_out, ws, nslot, scale,
+                        stream);
   return hipGetLastError();
 }
 
@@ -1065,9 +1247,10 @@ void launch_score_norm_small(const KvView &kv, int batch, int Hkv, const SelectW
 
 template <int D, bool BF16>
 hipError_t launch_select_xq_t(int batch, int block, int x, const void *q_sel,
-                              const KvView &kv, int Hq, int Hkv, const void *tail, int n_tail,
-                              const int32_t *k_per_seq, int k_max, int32_t *idx_out,
-                              const SelectWs &ws, hipStream_t stream) {
+                              const KvView &kv, int Hq, int Hkv, const void *tail,
+                              const void *tail_v, int n_tail, const int32_t *k_per_seq,
+                              int k_max, int32_t *idx_out, void *o_out, const SelectWs &ws,
+                              hipStream_t stream) {
   const int V = x * (Hq / Hkv);
   const double scale = 1.0 / sqrt((double)D);
   const int nslot = ws.nchunk + 1;
@@ -1094,6 +1277,9 @@ hipError_t launch_select_xq_t(int batch, int block, int x, const void *q_sel,
   }
   topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
       kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
+  if (o_out)
+    launch_out<D, BF16>(kv, batch, Hq, Hkv, V, tail, tail_v, n_tail, o_out, ws, nslot, scale,
+                        stream);
   return hipGetLastError();
 }
 
@@ -1113,12 +1299,14 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
   const size_t o_part = off; off = align256(off + bh * (nchunk + 1) * G * 2 * sizeof(double));
   const size_t o_keys = off; off = align256(off + bh * S_pad * sizeof(uint64_t));
   const size_t o_hist = off; off = align256(off + bh * kHistBins * sizeof(uint32_t));
+  const size_t o_opart = off; off = align256(off + bh * (nchunk + 1) * G * d * sizeof(float));
   if (layout) {
     layout->qbar = reinterpret_cast<double *>(base + o_qbar);
     layout->espill = reinterpret_cast<double *>(base + o_z);
     layout->part = reinterpret_cast<double *>(base + o_part);
     layout->keys = reinterpret_cast<uint64_t *>(base + o_keys);
     layout->hist = reinterpret_cast<uint32_t *>(base + o_hist);
+    layout->opart = reinterpret_cast<float *>(base + o_opart);
     layout->S_pad = S_pad;
     layout->nchunk = nchunk;
   }
@@ -1126,23 +1314,24 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
 }
 
 hipError_t launch_select_xq(const herald_heads &hd, int batch, int block, int x,
-                            const void *q_sel, const KvView &kv, const void *tail, int n_tail,
-                            const int32_t *k_per_seq, int k_max, int32_t *idx_out,
-                            const SelectWs &ws, hipStream_t stream) {
+                            const void *q_sel, const KvView &kv, const void *tail,
+                            const void *tail_v, int n_tail, const int32_t *k_per_seq, int k_max,
+                            int32_t *idx_out, void *o_out, const SelectWs &ws,
+                            hipStream_t stream) {
   const bool bf = hd.dtype == HERALD_BF16;
   const int Hq = hd.num_q_heads, Hkv = hd.num_kv_heads;
 #define HERALD_SELX(D_, BF_)                                                              \
   if (hd.head_dim == D_ && bf == BF_)                                                     \
-    return launch_select_xq_t<D_, BF_>(batch, block, x, q_sel, kv, Hq, Hkv, tail, n_tail, \
-                                       k_per_seq, k_max, idx_out, ws, stream);
+    return launch_select_xq_t<D_, BF_>(batch, block, x, q_sel, kv, Hq, Hkv, tail, tail_v, \
+                                       n_tail, k_per_seq, k_max, idx_out, o_out, ws, stream);
   HERALD_SELX(64, true) HERALD_SELX(64, false) HERALD_SELX(128, true) HERALD_SELX(128, false)
 #undef HERALD_SELX
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_select(const herald_heads &hd, int batch, int block, const void *q_sel,
-                         const KvView &kv, const void *tail, int n_tail,
-                         const int32_t *k_per_seq, int k_max, int32_t *idx_out,
+                         const KvView &kv, const void *tail, const void *tail_v, int n_tail,
+                         const int32_t *k_per_seq, int k_max, int32_t *idx_out, void *o_out,
                          const SelectWs &ws, hipStream_t stream) {
   const int G = hd.num_q_heads / hd.num_kv_heads;
   const bool bf = hd.dtype == HERALD_BF16;
@@ -1150,11 +1339,11 @@ hipError_t launch_select(const herald_heads &hd, int batch, int block, const voi
 #define HERALD_SEL(D_, G_)                                                              \
   if (hd.head_dim == D_ && G == G_)                                                     \
     return bf ? launch_select_t<D_, G_, true>(batch, block, q_sel, kv, Hq, Hkv, tail,   \
-                                              n_tail, k_per_seq, k_max, idx_out, ws,    \
-                                              stream)                                   \
+                                              tail_v, n_tail, k_per_seq, k_max, idx_out, \
+                                              o_out, ws, stream)                         \
               : launch_select_t<D_, G_, false>(batch, block, q_sel, kv, Hq, Hkv, tail,  \
-                                               n_tail, k_per_seq, k_max, idx_out, ws,   \
-                                               stream);
+                                               tail_v, n_tail, k_per_seq, k_max,         \
+                                               idx_out, o_out, ws, stream);
   HERALD_SEL(64, 1) HERALD_SEL(64, 2) HERALD_SEL(64, 4) HERALD_SEL(64, 8)
   HERALD_SEL(128, 1) HERALD_SEL(128, 2) HERALD_SEL(128, 4) HERALD_SEL(128, 8)
 #undef HERALD_SEL

@@ -86,6 +86,10 @@ def lib():
     L.herald_select_draft.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i32, c_p,
                                       ctypes.POINTER(KV), c_p, c_i32, c_p, c_i32, c_p, c_p,
                                       c_sz, c_p]
+    L.herald_select_attn.restype = ctypes.c_int
+    L.herald_select_attn.argtypes = [ctypes.POINTER(Heads), c_i32, c_i32, c_i32, c_p,
+                                     ctypes.POINTER(KV), c_p, c_p, c_i32, c_p, c_i32, c_p, c_p,
+                                     c_p, c_sz, c_p]
     L.herald_gather.restype = ctypes.c_int
     L.herald_gather.argtypes = [ctypes.POINTER(Heads), c_i32, ctypes.POINTER(KV), c_p, c_p,
                                 c_i32, ctypes.POINTER(Pool), c_i32, c_p]
@@ -110,7 +114,7 @@ def lib():
 
 EXPORTS = ("herald_status_string", "herald_budget_tokens", "herald_select_workspace",
            "herald_select", "herald_select_xq_workspace", "herald_select_xq",
-           "herald_select_draft",
+           "herald_select_draft", "herald_select_attn",
            "herald_gather", "herald_block_attn_workspace",
            "herald_block_attn", "herald_block_attn_groups", "herald_decode_block_workspace",
            "herald_decode_block")
@@ -222,6 +226,17 @@ def select_draft(hd: Heads, batch: int, block: int, x: int, q_sel, kv: KV, draft
                                    ctypes.byref(kv), _ptr(draft_k), n_draft, _ptr(k_per_seq),
                                    k_max, _ptr(idx_out), _ptr(ws), nbytes, _stream(stream))
     _check("herald_select_draft", st)
+
+
+def select_attn(hd: Heads, batch: int, block: int, x: int, q_sel, kv: KV, draft_k, draft_v,
+                n_draft: int, k_per_seq, k_max: int, idx_out, o_out, ws,
+                ws_bytes: int | None = None, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().herald_select_attn(ctypes.byref(hd), batch, block, x, _ptr(q_sel),
+                                  ctypes.byref(kv), _ptr(draft_k), _ptr(draft_v), n_draft,
+                                  _ptr(k_per_seq), k_max, _ptr(idx_out), _ptr(o_out), _ptr(ws),
+                                  nbytes, _stream(stream))
+    _check("herald_select_attn", st)
 
 
 def gather(hd: Heads, batch: int, kv: KV, idx, k_per_seq, k_max: int, dst: Pool,

@@ -148,6 +148,21 @@ def test_select_draft_validation():
     assert _select_draft(draft=None, n_draft=0) == H.ERR_WORKSPACE  # no draft: fine to here
 
 
+def test_select_attn_validation():
+    hd = H.heads(32, 8, 128, "bf16")
+
+    def call(o=FAKE, dv=FAKE, n=32, v=FAKE, wsb=10):
+        kv = _kv(v=v)
+        return H.lib().herald_select_attn(ctypes.byref(hd), 2, 32, 1, FAKE, ctypes.byref(kv),
+                                          FAKE, dv, n, FAKE, 52, FAKE, o, FAKE * 256, wsb, None)
+    assert call() == H.ERR_WORKSPACE                  # valid up to the workspace
+    assert call(o=None) == H.ERR_INVALID_ARG
+    assert call(o=FAKE + 8) == H.ERR_INVALID_ARG
+    assert call(dv=None) == H.ERR_INVALID_ARG         # the draft's V is read
+    assert call(dv=None, n=0) == H.ERR_WORKSPACE
+    assert call(v=None) == H.ERR_INVALID_ARG          # the cache's V is read
+
+
 def test_block_attn_groups_validation():
     hd = H.heads(32, 8, 128, "bf16")
     kv = _kv(max_seq_len=1638)

@@ -9,8 +9,8 @@ import torch
 import oracle
 from paper_2606_21633_amd import herald as H
 from paper_2606_21633_amd import synth
-from tests.gpu_util import (DEV, Staged, assert_same_selection, boundary_gap, budgets,
-                            seq_kv_host, to_dev)
+from tests.gpu_util import (DEV, Staged, assert_same_selection, boundary_gap, budgets, f64,
+                            seq_kv_host, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -263,6 +263,74 @@ def test_select_draft_paged_and_strong_draft_changes_selection():
     assert near == 0
     _, without = check_select_draft(wl, 1, 0)
     assert (with_d != without).any()
+
+
+# ---------------------------------------------------------------- attention output
+
+OUT_TOL = {"bf16": 2e-2, "f32": 1e-5}
+
+
+def check_select_attn(wl, x, n_draft, seqs=None, seed=6):
+    inp = synth.make_host(wl)
+    rng = np.random.default_rng(seed)
+    st = Staged(wl, inp)
+    lens = inp["seq_lens"]
+    kps_h = budgets(lens, *wl.budget)
+    k_max = int(max(1, min(kps_h.max(), lens.max())))
+    d, Hkv, Hq = wl.head_dim, wl.num_kv_heads, wl.num_q_heads
+    dk = synth._to_dtype((rng.standard_normal((wl.batch, max(n_draft, 1), Hkv, d)) * 2.0)
+                         .astype(np.float32), wl.dtype)
+    dv = synth._to_dtype(rng.standard_normal((wl.batch, max(n_draft, 1), Hkv, d))
+                         .astype(np.float32), wl.dtype)
+    tdk, tdv, kps = to_dev(dk), to_dev(dv), to_dev(kps_h)
+    nrow = max(x, 1)
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    o = torch.zeros((wl.batch, nrow, Hq, d), dtype=tdt, device=DEV)
+    idx = torch.full((wl.batch, Hkv, k_max), -7, dtype=torch.int32, device=DEV)
+    ws = H.workspace(H.select_xq_workspace(st.hd, wl.batch, nrow, st.S_max), DEV)
+    H.select_attn(st.hd, wl.batch, wl.block, x, st.q_sel, st.kv, tdk, tdv, n_draft, kps, k_max,
+                  idx, o, ws)
+    torch.cuda.synchronize()
+    got, got_o = idx.cpu().numpy(), f64(to_host(o))
+    near, worst = 0, 0.0
+    for b in (range(wl.batch) if seqs is None else seqs):
+        S = int(lens[b])
+        k = int(min(max(kps_h[b], 0), S, k_max))
+        kh, vh = seq_kv_host(inp, b)
+        tk, tv = (dk[b, :n_draft], dv[b, :n_draft]) if n_draft else (None, None)
+        idx_o, shat, o_o = oracle.select_draft(inp["q_sel"][b], kh, tk, k, x, V=vh, tail_v=tv)
+        for h in range(Hkv):
+            near += assert_same_selection(got[b, h, :k], idx_o[h], shat[h], k)
+        err = float(np.abs(got_o[b] - o_o).max())
+        worst = max(worst, err)
+        assert err <= OUT_TOL[wl.dtype], f"seq {b}: attention output max abs err {err}"
+    print(f"[select_attn] {wl.name} x={x} n_draft={n_draft}: near-ties={near} "
+          f"max abs err {worst:.3g}")
+    return near
+
+
+@pytest.mark.parametrize("x,n_draft", [(0, 0), (0, 32), (1, 32), (3, 5), (8, 0)])
+def test_select_attention_output(x, n_draft):
+    wl = XQ.replace(name=f"attn out x{x}", num_q_heads=8, seed=120 + x + n_draft)
+    assert check_select_attn(wl, x, n_draft) == 0
+
+
+@pytest.mark.parametrize("G,d,dtype,x", [(1, 64, "f32", 0), (2, 128, "f32", 2), (8, 64, "bf16", 1),
+                                         (4, 64, "bf16", 32)])
+def test_select_attention_output_group_and_dims(G, d, dtype, x):
+    wl = XQ.replace(name=f"attn out G{G} d{d} {dtype}", num_q_heads=2 * G, head_dim=d,
+                    dtype=dtype, seed=130 + G + d + x)
+    assert check_select_attn(wl, x, 16) == 0
+
+
+def test_select_attention_output_paged():
+    wl = XQ.replace(name="attn out paged", batch=4, page_size=16, seq_len=3000, seq_len_lo=17,
+                    num_q_heads=8, seed=34)
+    assert check_select_attn(wl, 1, 32) == 0
+
+
+def test_select_attention_output_layer_32k_sampled():
+    assert check_select_attn(synth.LAYER_32K, 1, 32, seqs=[0, 9]) == 0
 
 
 def test_select_layer_32k_workload_full():
