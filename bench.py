@@ -488,8 +488,24 @@ def bench_xq_sweep(args):
                      "workspace_GB": round(ws.numel() / 1e9, 3)})
         del ws
         torch.cuda.empty_cache()
+    # the paper's selection: centre query, block n's draft KV as normalisation
+    # tail, plus the attention output handed to the FFN
+    ws = H.workspace(H.select_xq_workspace(hd, b, 1, S), dev)
+    dk = torch.randn((b, B, Hkv, d), device=dev).to(torch.bfloat16)
+    dvv = torch.randn((b, B, Hkv, d), device=dev).to(torch.bfloat16)
+    o = torch.empty((b, 1, Hq, d), dtype=torch.bfloat16, device=dev)
+    ms_d = _timed(lambda: H.select_draft(hd, b, B, 1, q_sel, kv, dk, B, kps, k_b, idx, ws),
+                  args.reps, s)
+    ms_o = _timed(lambda: H.select_attn(hd, b, B, 1, q_sel, kv, dk, dvv, B, kps, k_b, idx, o, ws),
+                  args.reps, s)
+    rows.append({"x": "1 + draft tail", "ms": round(ms_d, 4),
+                 "scan_GBps": round(kbytes / ms_d / 1e6, 1)})
+    rows.append({"x": "1 + draft tail + attention output", "ms": round(ms_o, 4),
+                 "scan_GBps": round(kbytes / ms_o / 1e6, 1),
+                 "kv_bytes_GBps": round(2 * kbytes / ms_o / 1e6, 1)})
+    del ws
     for r in rows:
-        if r["x"] != "mean":
+        if isinstance(r["x"], int):
             r["speedup_vs_x32"] = round(per_x[32] / r["ms"], 2)
     res = {"metric": "selection throughput vs query count x (x = 1 over x = 32)",
            "value": round(per_x[32] / per_x[1], 3), "unit": "x", "n_gpus": 1,

@@ -806,22 +806,27 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
 // output accumulator that the paper's fused kernel keeps beside (m, l),
 // sec. IV-B.4), from the spilled fp64 scores and the merged statistics, with
 // fp32 weights and fp32 accumulation. out_kernel: one workgroup per (chunk,
-// KV head, sequence) writes the chunk's partial sum [V][D]; thread t takes
-// elements 2 (t % (D/2)) + {0, 1} of score rows t / (D/2) + VS j (VS = 512 / D
-// slots, NV rows per slot and pass); the weights of 32 cached rows at a time
-// are formed once in LDS and read by every thread of a wave at one address.
+// KV head, sequence) writes the chunk's partial sum [V][D]. A cached row is
+// read as D / EPL 16-byte pieces by as many consecutive threads (its row
+// slot); each thread keeps NV score rows x EPL elements of one piece position
+// and loads the pieces of a 128-row tile all at once; the weights of the tile
+// are formed once in LDS. At the end the row slots are summed in a fixed
+// order: shuffles within a wave, then the four waves through LDS.
 template <int D, int NV, bool BF16>
 __global__ __launch_bounds__(256) void out_kernel(KvView kv, const double *__restrict__ zspill,
                                                   const double *__restrict__ part,
                                                   float *__restrict__ opart, int Hkv, int V,
                                                   int64_t S_pad, int nslot) {
   constexpr int ELT = BF16 ? 2 : 4;
-  constexpr int EP = D / 2;       // element pairs of a row
-  constexpr int VS = 256 / EP;    // score-row slots
-  constexpr int VB = VS * NV;     // score rows per pass
-  constexpr int TR = 32;          // cached rows per weight tile
+  constexpr int EPL = 16 / ELT;   // elements per 16-byte piece
+  constexpr int SEG = D / EPL;    // pieces per cached row
+  constexpr int RS = 256 / SEG;   // cached rows per step (row slots)
+  constexpr int WRS = 64 / SEG;   // row slots per wave
+  constexpr int TR = 128;         // cached rows per weight tile
+  constexpr int SPT = TR / RS;    // steps per tile
   __shared__ double sm[kMaxScoreRows], sinv[kMaxScoreRows];
-  __shared__ float wt[TR][VB];
+  __shared__ float wt[TR][NV];
+  __shared__ float red[4][NV][D];
   const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
@@ -835,53 +840,70 @@ __global__ __launch_bounds__(256) void out_kernel(KvView kv, const double *__res
     if (lane == 0) { sm[v] = m; sinv[v] = inv; }
   }
   __syncthreads();
-  const int ep = threadIdx.x % EP, vs = threadIdx.x / EP;
+  const int seg = threadIdx.x % SEG, rslot = threadIdx.x / SEG;
   const int64_t c1 = min(c0 + (int64_t)kScoreChunk, S);
-  for (int vb0 = 0; vb0 < V; vb0 += VB) {
-    float acc[NV][2];
+  for (int vb0 = 0; vb0 < V; vb0 += NV) {
+    float acc[NV][EPL];
 #pragma unroll
-    for (int j = 0; j < NV; ++j) acc[j][0] = acc[j][1] = 0.f;
+    for (int j = 0; j < NV; ++j)
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) acc[j][u] = 0.f;
     for (int64_t r0 = c0; r0 < c1; r0 += TR) {
-      for (int i = threadIdx.x; i < TR * VB; i += 256) {
-        const int rr = i / VB, v = vb0 + i % VB;
+      for (int i = threadIdx.x; i < TR * NV; i += 256) {
+        const int rr = i / NV, v = vb0 + i % NV;
         const int64_t s = r0 + rr;
         float w = 0.f;
         if (s < c1 && v < V)
           w = (float)(exp(zspill[(bh * S_pad + s) * V + v] - sm[v]) * sinv[v]);
-        wt[rr][i % VB] = w;
+        wt[rr][i % NV] = w;
       }
       __syncthreads();
-      const int nr = (int)min((int64_t)TR, c1 - r0);
-      for (int rr = 0; rr < nr; ++rr) {
-        const char *row = kv.v + kv_row(kv, b, h, r0 + rr) * ELT;
-        float x0, x1;
-        if (BF16) {
-          const uint32_t w2 = *reinterpret_cast<const uint32_t *>(row + 4 * ep);
-          x0 = bf16_lo(w2);
-          x1 = bf16_hi(w2);
-        } else {
-          const float2 f2 = *reinterpret_cast<const float2 *>(row + 8 * ep);
-          x0 = f2.x;
-          x1 = f2.y;
-        }
+      uint4 pc[SPT];
+#pragma unroll
+      for (int st = 0; st < SPT; ++st) {
+        const int64_t s = r0 + st * RS + rslot;
+        pc[st] = make_uint4(0u, 0u, 0u, 0u);
+        if (s < c1) pc[st] = ldg16(kv.v + kv_row(kv, b, h, s) * ELT + seg * 16);
+      }
+#pragma unroll
+      for (int st = 0; st < SPT; ++st) {
+        const int rr = st * RS + rslot;
+        const uint32_t w4[4] = {pc[st].x, pc[st].y, pc[st].z, pc[st].w};
+        float x[EPL];
+#pragma unroll
+        for (int u = 0; u < EPL; ++u)
+          x[u] = BF16 ? ((u & 1) ? bf16_hi(w4[u >> 1]) : bf16_lo(w4[u >> 1]))
+                      : __uint_as_float(w4[u]);
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
-          const float w = wt[rr][vs + VS * j];
-          acc[j][0] = fmaf(w, x0, acc[j][0]);
-          acc[j][1] = fmaf(w, x1, acc[j][1]);
+          const float w = wt[rr][j];
+#pragma unroll
+          for (int u = 0; u < EPL; ++u) acc[j][u] = fmaf(w, x[u], acc[j][u]);
         }
       }
       __syncthreads();
     }
+    // row slots of a wave (lanes seg + SEG r) in a fixed tree, then the waves
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int v = vb0 + vs + VS * j;
-      if (v < V) {
-        float *o = opart + ((bh * nslot + chunk) * V + v) * D + 2 * ep;
-        o[0] = acc[j][0];
-        o[1] = acc[j][1];
-      }
+    for (int off = SEG; off < 64; off <<= 1)
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) acc[j][u] += __shfl_xor(acc[j][u], off, 64);
+    static_assert(WRS >= 1, "a wave holds at least one row slot");
+    if (lane < SEG)
+#pragma unroll
+      for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int u = 0; u < EPL; ++u) red[wave][j][seg * EPL + u] = acc[j][u];
+    __syncthreads();
+    for (int i = threadIdx.x; i < NV * D; i += 256) {
+      const int j = i / D, e = i % D, v = vb0 + j;
+      if (v < V)
+        opart[((bh * nslot + chunk) * V + v) * D + e] =
+            ((red[0][j][e] + red[1][j][e]) + red[2][j][e]) + red[3][j][e];
     }
+    __syncthreads();
   }
 }
 
@@ -1175,12 +1197,11 @@ void launch_out(const KvView &kv, int batch, int Hq, int Hkv, int V, const void 
                 const void *tail_v, int n_tail, void *o_out, const SelectWs &ws, int nslot,
                 double scale, hipStream_t stream) {
   const dim3 grid(ws.nchunk, Hkv, batch);
-  constexpr int VS = 512 / D;  // score-row slots of out_kernel
-  if (V <= VS)
-    out_kernel<D, 1, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
-                                                     ws.S_pad, nslot);
-  else if (V <= 4 * VS)
+  if (V <= 4)
     out_kernel<D, 4, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
+                                                     ws.S_pad, nslot);
+  else if (V <= 8)
+    out_kernel<D, 8, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
                                                      ws.S_pad, nslot);
   else
     out_kernel<D, 16, BF16><<<grid, 256, 0, stream>>>(kv, ws.espill, ws.part, ws.opart, Hkv, V,
