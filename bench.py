@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--select-x", type=int, default=0, choices=[0, 1],
                     help="36-layer workload: next-block representative query, 0 the mean of "
                          "the block's queries, 1 its centre row")
+    ap.add_argument("--graph", action="store_true",
+                    help="8B-class layer: replay the pipelined block from HIP graphs (one per "
+                         "pool parity, captured after the warm-up)")
     ap.add_argument("--dense", action="store_true",
                     help="denoise over the full cache (GPU-only dense baseline)")
     ap.add_argument("--reps", type=int, default=30, help="isolated kernel timing reps")
@@ -154,6 +157,24 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.graph:
+        # the whole block (lengths reset, both streams, join, append) as one
+        # graph per pool parity; the timed loop replays them alternately
+        graphs = []
+        for _ in range(2):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s_main):
+                step()
+            graphs.append(g)
+        torch.cuda.synchronize()
+
+        def step():   # noqa: F811 (the replaying step replaces the eager one)
+            with torch.cuda.stream(s_main):   # the timing events are on s_main
+                graphs[state["a"]].replay()
+            state["a"] = 1 - state["a"]
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
     print(f"[bench] timing {args.steps} pipelined blocks", file=sys.stderr, flush=True)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -263,6 +284,7 @@ def main():
         "config": {"workload": wl.name, "batch": b, "seq_len": S, "block": B, "steps": T,
                    "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "budget_tokens": k_b,
                    "layers": 1, "mode": "dense" if args.dense else "sparse",
+                   "graph": bool(args.graph),
                    "step": "one pipelined block: next-block selection on a second stream "
                            "overlapped with T denoising steps, join, append, swap"},
         # B*G query rows per KV head give 4*B*G*d flops per 4*d bytes of bf16 K+V

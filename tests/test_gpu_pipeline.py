@@ -53,7 +53,7 @@ def make_case(b=2, Hq=8, Hkv=2, d=128, B=8, T=2, L=2, nblocks=3, S_lo=900, S_hi=
 
 
 def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, dense_layers=(),
-            draft_layers=(), select_x=0):
+            draft_layers=(), select_x=0, graphs=False):
     b, Hq, Hkv, d, B, T, L = (case[x] for x in ("b", "Hq", "Hkv", "d", "B", "T", "L"))
     hd = H.heads(Hq, Hkv, d, "bf16")
     lens_h = case["lens"].copy()
@@ -70,6 +70,9 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
         L_["out"] = torch.zeros((T, b, B, Hq, d), dtype=torch.bfloat16, device=DEV)
         L_["out_draft"] = torch.zeros((b, B, Hq, d), dtype=torch.bfloat16, device=DEV)
         L_["blocks"] = [{n: to_dev(a) for n, a in blk.items()} for blk in lay["blocks"]]
+        # a graph keeps the input pointers it was captured with: fixed buffers
+        # that every block's inputs are copied into
+        L_["stage"] = {n: torch.empty_like(t) for n, t in L_["blocks"][0].items()}
         dl.append(L_)
     n_pool = [torch.zeros(b, dtype=torch.int32, device=DEV) for _ in range(2)]
     # initial selection per layer (prefill-time top-k) into pool 0
@@ -92,12 +95,18 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
     ws = H.workspace(H.decode_block_workspace(hd, b, B, S_bound, k_hi), DEV)
     outs = []
     a = 0
+    kn = torch.zeros(b, dtype=torch.int32, device=DEV)   # updated in place every block
+    graph = [None, None]
     for n in range(case["nblocks"]):
         kn_h = np.array([H.budget_tokens(int(s), num, den) for s in lens_h], np.int32)
-        kn = to_dev(kn_h)
+        kn.copy_(torch.from_numpy(kn_h))
         layers = []
         for l, L_ in enumerate(dl):
             blk = L_["blocks"][n]
+            if graphs:
+                for name, t in blk.items():
+                    L_["stage"][name].copy_(t)
+                blk = L_["stage"]
             layer = H.Layer(
                 H.pool_view(L_["k"], L_["v"]), H.pool_view(*L_["pools"][a]),
                 H.pool_view(*L_["pools"][1 - a]), blk["q"].data_ptr(), blk["bk"].data_ptr(),
@@ -113,9 +122,28 @@ def run_gpu(case, dense=False, one_stream=False, delay_main=0, num=1, den=20, de
         if delay_main:
             with torch.cuda.stream(s_main):
                 torch.cuda._sleep(delay_main)
-        H.decode_block(hd, layers, b, B, T, lens, int(lens_h.max()), n_pool[a], pcap,
-                       n_pool[1 - a], kn, int(kn_h.max()), dense, ws, s_main, s_retr)
+        # host-side arguments that a graph fixes: the largest S and k of the run
+        S_arg = int(lens_h.max()) if not graphs else S_bound - B
+        k_arg = int(kn_h.max()) if not graphs else k_hi
+        call = lambda: H.decode_block(hd, layers, b, B, T, lens, S_arg, n_pool[a], pcap,
+                                      n_pool[1 - a], kn, k_arg, dense, ws, s_main, s_retr)
+        if not graphs:
+            call()
+        elif graph[a] is None:
+            # capture this parity's block (the capture itself runs nothing),
+            # then replay it
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s_main):
+                call()
+            graph[a] = (g, layers)
+            torch.cuda.synchronize()
+            g.replay()
+        else:
+            graph[a][0].replay()
         torch.cuda.synchronize()
+        if graphs:   # eager work between replays
+            x = torch.randn(256, 256, device=DEV)
+            (x @ x).sum().item()
         outs.append([to_host(L_["out"]).copy() for L_ in dl])
         if draft_layers:
             outs[-1].append([to_host(L_["out_draft"]).copy() for L_ in dl])
@@ -331,3 +359,23 @@ def test_pipeline_36_layer_workload_shape_sampled():
                 worst = max(worst, err)
                 assert err <= TOL, f"layer {l} seq {i} block {n}: {err}"
     print(f"[pipeline 36L shape] max abs err {worst:.3g}")
+
+
+def test_pipeline_replayed_from_hip_graphs_matches_eager():
+    """One captured graph per pool parity (the active/idle pointers alternate),
+    replayed block after block with eager work (a matmul and a copy) between
+    replays: every replayed block's outputs, caches and pool lengths equal
+    those of the eager run bit for bit."""
+    case = make_case(seed=9, L=2, T=3, nblocks=4, drafts=True)
+    ref, ref_caches = run_gpu(case, draft_layers=(1,), select_x=1)
+    got, got_caches = run_gpu(case, draft_layers=(1,), select_x=1, graphs=True)
+    for n in range(case["nblocks"]):
+        for l in range(case["L"] + 1):
+            a, b = got[n][l], ref[n][l]
+            if isinstance(a, list):
+                for x, y in zip(a, b):
+                    assert x.tobytes() == y.tobytes(), (n, l)
+            else:
+                assert a.tobytes() == b.tobytes(), (n, l)
+    for (ka, va), (kb, vb) in zip(got_caches, ref_caches):
+        assert ka.tobytes() == kb.tobytes() and va.tobytes() == vb.tobytes()
