@@ -604,10 +604,12 @@ def bench_pipeline36(args):
             n_pool[0].fill_(k0)
         torch.cuda.synchronize()
         a, times = 0, []
+        kn = torch.zeros((b,), dtype=torch.int32, device=dev)
+        graphs = {}
         for n in range(nblk):
             S = int(lens_h[0])
             kn_h = H.budget_tokens(S, *wl.budget)
-            kn = torch.full((b,), kn_h, dtype=torch.int32, device=dev)
+            kn.fill_(kn_h)
             lay = [H.Layer(H.pool_view(Ly["k"], Ly["v"]), H.pool_view(*Ly["pools"][a]),
                            H.pool_view(*Ly["pools"][1 - a]), Ly["q"].data_ptr(),
                            Ly["bk"].data_ptr(), Ly["bv"].data_ptr(), Ly["dk"].data_ptr(),
@@ -619,11 +621,23 @@ def bench_pipeline36(args):
                     Lr.q_draft, Lr.draft_k = Ly["qd"].data_ptr(), Ly["ddk"].data_ptr()
                     Lr.draft_v, Lr.out_draft = Ly["ddv"].data_ptr(), Ly["od"].data_ptr()
             torch.cuda.synchronize()
+            if args.graph and n >= args.warmup and a not in graphs:
+                # one graph per pool parity, host bounds set to the run's maxima
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=s_main):
+                    H.decode_block(hd, lay, b, B, T, lens, cap - B, n_pool[a], pcap,
+                                   n_pool[1 - a], kn, k_hi, dense, ws, s_main, s_retr)
+                graphs[a] = (g, lay)
+                torch.cuda.synchronize()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(s_main)
-            H.decode_block(hd, lay, b, B, T, lens, S, n_pool[a], pcap, n_pool[1 - a], kn,
-                           kn_h, dense, ws, s_main, s_retr)
+            if a in graphs:
+                with torch.cuda.stream(s_main):
+                    graphs[a][0].replay()
+            else:
+                H.decode_block(hd, lay, b, B, T, lens, S, n_pool[a], pcap, n_pool[1 - a], kn,
+                               kn_h, dense, ws, s_main, s_retr)
             e1.record(s_main)
             torch.cuda.synchronize()
             print(f"[bench] {'dense' if dense else 'sparse'} block {n}: "
@@ -645,6 +659,7 @@ def bench_pipeline36(args):
            "config": {"workload": wl.name, "layers": L, "batch": b, "seq_len": S0, "block": B,
                       "steps": T, "budget": "5%", "dense_layers": nd,
                       "drafts": bool(args.drafts), "select_x": args.select_x,
+                      "graph": bool(args.graph),
                       "step": "one block: next-block selection of "
                       "all layers on the retrieval stream, T x L denoising steps on the main "
                       "stream, join, append, swap"},
