@@ -14,7 +14,7 @@ namespace {
 constexpr int kGatherThreads = 256;
 constexpr int kRowsPerWg = 64;
 
-template <int RB>
+template <int RB, bool PAGED>
 __global__ __launch_bounds__(kGatherThreads) void gather_kernel(
     KvView kv, const int32_t *__restrict__ idx, const int32_t *__restrict__ kps,
     int k_max, PoolView dst, int dst_row0, int Hkv, int elt) {
@@ -27,19 +27,36 @@ __global__ __launch_bounds__(kGatherThreads) void gather_kernel(
   if (j0 >= k) return;
   const int64_t bh = (int64_t)b * Hkv + h;
   const int lr = threadIdx.x / LPR, lc = threadIdx.x % LPR;
+  constexpr int NIT = kRowsPerWg / RPI;
+  // every index, then every row load, then every store: NIT rows of K and V
+  // in flight per thread (a row whose index is out of range, or past k, is
+  // skipped; herald_select produces none of the former)
+  int64_t s[NIT];
 #pragma unroll
-  for (int it = 0; it < kRowsPerWg / RPI; ++it) {
+  for (int it = 0; it < NIT; ++it) {
     const int j = j0 + it * RPI + lr;
-    if (j >= k) break;
-    const int64_t s = idx[bh * k_max + j];
-    if (s < 0 || s >= S) continue;  // not produced by herald_select
-    const int64_t src = kv_row(kv, b, h, s) * elt + lc * 16;
+    const int32_t x = idx[bh * k_max + min(j, k - 1)];  // (row k - 1 re-read, unused)
+    s[it] = j < k ? (int64_t)x : -1;
+  }
+  // a skipped row loads row 0 of the sequence (in bounds) and stores nothing
+  uint4 kx[NIT], vx[NIT];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int64_t row = s[it] >= 0 && s[it] < S ? s[it] : 0;
+    const int64_t src =
+        (PAGED ? kv_row(kv, b, h, row) : (int64_t)b * kv.sb + (int64_t)h * kv.sh + row * kv.ss) *
+            elt + lc * 16;
+    kx[it] = ldg16(kv.k + src);
+    vx[it] = ldg16(kv.v + src);
+  }
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    if (s[it] < 0 || s[it] >= S) continue;
+    const int j = j0 + it * RPI + lr;
     const int64_t d = ((int64_t)b * dst.sb + (int64_t)h * dst.sh +
                        (int64_t)(dst_row0 + j) * dst.ss) * elt + lc * 16;
-    const uint4 kx = ldg16(kv.k + src);
-    const uint4 vx = ldg16(kv.v + src);
-    *reinterpret_cast<uint4 *>(dst.k + d) = kx;
-    *reinterpret_cast<uint4 *>(dst.v + d) = vx;
+    *reinterpret_cast<uint4 *>(dst.k + d) = kx[it];
+    *reinterpret_cast<uint4 *>(dst.v + d) = vx[it];
   }
 }
 
@@ -51,15 +68,23 @@ hipError_t launch_gather(const herald_heads &hd, int batch, const KvView &kv,
   const int elt = hd.dtype == HERALD_BF16 ? 2 : 4;
   const int rb = hd.head_dim * elt;
   const dim3 grid((k_max + kRowsPerWg - 1) / kRowsPerWg, hd.num_kv_heads, batch);
+  const bool paged = kv.pt != nullptr;
+#define HERALD_GATHER(RB_)                                                                    \
+  case RB_:                                                                                  \
+    if (paged)                                                                               \
+      gather_kernel<RB_, true><<<grid, kGatherThreads, 0, stream>>>(                          \
+          kv, idx, k_per_seq, k_max, dst, dst_row0, hd.num_kv_heads, elt);                   \
+    else                                                                                     \
+      gather_kernel<RB_, false><<<grid, kGatherThreads, 0, stream>>>(                         \
+          kv, idx, k_per_seq, k_max, dst, dst_row0, hd.num_kv_heads, elt);                   \
+    break;
   switch (rb) {
-    case 128: gather_kernel<128><<<grid, kGatherThreads, 0, stream>>>(
-                  kv, idx, k_per_seq, k_max, dst, dst_row0, hd.num_kv_heads, elt); break;
-    case 256: gather_kernel<256><<<grid, kGatherThreads, 0, stream>>>(
-                  kv, idx, k_per_seq, k_max, dst, dst_row0, hd.num_kv_heads, elt); break;
-    case 512: gather_kernel<512><<<grid, kGatherThreads, 0, stream>>>(
-                  kv, idx, k_per_seq, k_max, dst, dst_row0, hd.num_kv_heads, elt); break;
+    HERALD_GATHER(128)
+    HERALD_GATHER(256)
+    HERALD_GATHER(512)
     default: return hipErrorInvalidValue;
   }
+#undef HERALD_GATHER
   return hipGetLastError();
 }
 
