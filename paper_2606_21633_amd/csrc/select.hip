@@ -127,6 +127,24 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
 // half of the head dimension with the qbar half it holds in scalar registers.
 // The halves are added in a fixed order (low half + high half); the online
 // softmax statistics of the G heads are split between the two waves.
+// Page numbers of the pages that hold rows [c0, c0 + kScoreChunk) of
+// sequence b, staged in LDS by the workgroup (paged views): a tile's page
+// lookup is then an LDS read instead of a global load that its row loads wait
+// for. Pages hold at least 8 rows, so a chunk spans at most kChunkPages pages;
+// entries of pages past the sequence's rows (never read) are 0.
+constexpr int kChunkPages = kScoreChunk / 8;
+__device__ __forceinline__ void stage_chunk_pages(const KvView &kv, int b, int64_t c0,
+                                                  int64_t S, int32_t *spt) {
+  const int shift = kv.page_shift;
+  const int64_t p0 = c0 >> shift;
+  const int n = shift >= 11 ? 1 : (kScoreChunk >> shift);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int64_t pg = p0 + i;
+    spt[i] = pg < kv.max_pages && (pg << shift) < S ? kv.pt[(int64_t)b * kv.max_pages + pg] : 0;
+  }
+  __syncthreads();
+}
+
 template <int D, int G, bool BF16, bool PAGED>
 __global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
                                                        const double *__restrict__ qbar,
@@ -167,9 +185,11 @@ __global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
   const int g0 = G > 1 ? half * GH : 0;
   const bool keeps = G > 1 || half == 0;
 
+  __shared__ int32_t spt[PAGED ? kChunkPages : 1];
+  if constexpr (PAGED) stage_chunk_pages(kv, b, c0, S, spt);
   auto row_addr = [&](int64_t s_base, int64_t s) -> const char * {
     if (PAGED) {
-      const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s_base >> kv.page_shift)];
+      const int64_t page = spt[(s_base >> kv.page_shift) - (c0 >> kv.page_shift)];
       return kv.k + (page * kv.sp + (int64_t)h * kv.sh +
                      (s & ((1 << kv.page_shift) - 1)) * kv.ss) * ELT + lc * 16;
     }
@@ -362,9 +382,11 @@ __global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
   const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + lc * 16;
   // row s of a load whose first row s_base is uniform (a load never crosses
   // a page: pages hold at least 8 rows and loads start at multiples of RPL)
+  __shared__ int32_t spt[PAGED ? kChunkPages : 1];
+  if constexpr (PAGED) stage_chunk_pages(kv, b, c0, S, spt);
   auto row_addr = [&](int64_t s_base, int64_t s) -> const char * {
     if (PAGED) {
-      const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s_base >> kv.page_shift)];
+      const int64_t page = spt[(s_base >> kv.page_shift) - (c0 >> kv.page_shift)];
       return kv.k + (page * kv.sp + (int64_t)h * kv.sh +
                      (s & ((1 << kv.page_shift) - 1)) * kv.ss) * ELT + lc * 16;
     }
@@ -647,9 +669,11 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
 
   const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + kq * 16;
   // 16-byte piece p of cached row s (the lane's slot): row-by-row page lookup
+  __shared__ int32_t spt[PAGED ? kChunkPages : 1];
+  if constexpr (PAGED) stage_chunk_pages(kv, b, c0, S, spt);
   auto row_ptr = [&](int64_t s) -> const char * {
     if (PAGED) {
-      const int64_t page = kv.pt[(int64_t)b * kv.max_pages + (s >> kv.page_shift)];
+      const int64_t page = spt[(s >> kv.page_shift) - (c0 >> kv.page_shift)];
       return kv.k + (page * kv.sp + (int64_t)h * kv.sh +
                      (s & ((1 << kv.page_shift) - 1)) * kv.ss) * ELT + kq * 16;
     }

@@ -61,6 +61,17 @@ def test_select_ragged_paged():
     assert check_select(wl) == 0
 
 
+@pytest.mark.parametrize("page_size,G", [(8, 4), (64, 8), (4096, 4), (4096, 8), (8, 1)])
+def test_select_paged_page_sizes(page_size, G):
+    # the page-table slice of each scoring chunk is staged per workgroup: pages
+    # of 8 rows (256 per chunk), 64, and pages longer than a chunk (one entry);
+    # G = 8 takes the FMA scoring kernel, G <= 4 the MFMA one
+    wl = SMALL.replace(name=f"paged P{page_size} G{G}", batch=4, num_q_heads=2 * G,
+                       page_size=page_size, seq_len=9000 if page_size > 2048 else 5000,
+                       seq_len_lo=17, seed=40 + page_size % 97 + G)
+    assert check_select(wl) == 0
+
+
 @pytest.mark.parametrize("kps,k_max", [([1, 1, 1], 1), ([0, 5, 2000], 2000),
                                         ([10 ** 6, 3, 7], 4000), ([-3, 700, 699], 700),
                                         ([5000, 5000, 5000], 5000)])
@@ -169,10 +180,12 @@ def test_select_xq_group_and_dims(G, d, dtype, x):
     assert check_select_xq(wl, x) == 0
 
 
-@pytest.mark.parametrize("x", [1, 6])
-def test_select_xq_paged_ragged(x):
-    wl = XQ.replace(name="xq paged", batch=5, page_size=16, seq_len=3000, seq_len_lo=17,
-                    num_q_heads=8, seed=31 + x)
+@pytest.mark.parametrize("x,page_size", [(1, 16), (6, 16), (6, 8), (6, 4096), (1, 4096)])
+def test_select_xq_paged_ragged(x, page_size):
+    # pages of 8 rows (the smallest), 16, and pages longer than a scoring chunk
+    wl = XQ.replace(name=f"xq paged P{page_size}", batch=5, page_size=page_size,
+                    seq_len=9000 if page_size > 2048 else 5000, seq_len_lo=17, num_q_heads=8,
+                    seed=31 + x + page_size % 89)
     assert check_select_xq(wl, x) == 0
 
 
