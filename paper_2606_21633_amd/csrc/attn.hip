@@ -486,17 +486,37 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(
   const int r = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
   if (r >= M) return;
   const int64_t p0 = ((int64_t)b * Hkv + h) * nsplit;
-  // part_ml holds (max * scale * log2(e), sum) per row and split
+  // part_ml holds (max * scale * log2(e), sum) per row and split. Splits are
+  // read eight at a time with every load of a group issued before its
+  // arithmetic; the sums run over the splits in index order.
+  constexpr int GRP = 8;
   float mx = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, part_ml[(p0 + s) * M + r].x);
+  for (int s0 = 0; s0 < nsplit; s0 += GRP) {
+    float2 ml[GRP];
+#pragma unroll
+    for (int u = 0; u < GRP; ++u)
+      ml[u] = s0 + u < nsplit ? part_ml[(p0 + s0 + u) * M + r] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+    for (int u = 0; u < GRP; ++u) mx = fmaxf(mx, ml[u].x);
+  }
   float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float2 ml = part_ml[(p0 + s) * M + r];
-    if (ml.x == -INFINITY) continue;
-    const float w = __builtin_amdgcn_exp2f(ml.x - mx);
-    const float4 v = *reinterpret_cast<const float4 *>(part_o + ((p0 + s) * M + r) * D + d0);
-    den += ml.y * w;
-    n0 += v.x * w; n1 += v.y * w; n2 += v.z * w; n3 += v.w * w;
+  for (int s0 = 0; s0 < nsplit; s0 += GRP) {
+    float2 ml[GRP];
+    float4 v[GRP];
+#pragma unroll
+    for (int u = 0; u < GRP; ++u) {
+      const bool in = s0 + u < nsplit;
+      const int64_t sp = p0 + (in ? s0 + u : 0);
+      ml[u] = in ? part_ml[sp * M + r] : make_float2(-INFINITY, 0.f);
+      v[u] = *reinterpret_cast<const float4 *>(part_o + (sp * M + r) * D + d0);
+    }
+#pragma unroll
+    for (int u = 0; u < GRP; ++u) {
+      if (ml[u].x == -INFINITY) continue;
+      const float w = __builtin_amdgcn_exp2f(ml[u].x - mx);
+      den += ml[u].y * w;
+      n0 += v[u].x * w; n1 += v[u].y * w; n2 += v[u].z * w; n3 += v[u].w * w;
+    }
   }
   const float inv = 1.f / den;
   const int g = r / block, i = r % block;

@@ -97,6 +97,12 @@ def test_attn_bf16_ragged_tiles(n_ctx):
     run_attn("bf16", len(n_ctx), 32, 8, 128, 32, n_ctx, seed=len(n_ctx))
 
 
+def test_attn_bf16_many_key_splits():
+    """One sequence and one KV head over 20000 context rows: the plan splits
+    the keys 128 ways, so the combine merges its partials in 16 groups."""
+    run_attn("bf16", 1, 4, 1, 128, 32, [20000], seed=12)
+
+
 def test_attn_bf16_layer_32k_pool_shape():
     """The denoising step of the 8B-class 32K layer: 16 sequences, 1638 pool
     rows + 32 block rows per KV head; 4 sequences checked by the oracle."""
