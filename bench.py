@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="8B-class layer: replay the pipelined block from HIP graphs (one per "
                          "pool parity, captured after the warm-up)")
+    ap.add_argument("--serial", action="store_true",
+                    help="one stream: the next block's selection and gather run on the main "
+                         "stream ahead of the denoising steps instead of beside them")
     ap.add_argument("--dense", action="store_true",
                     help="denoise over the full cache (GPU-only dense baseline)")
     ap.add_argument("--reps", type=int, default=30, help="isolated kernel timing reps")
@@ -135,7 +138,7 @@ def main():
     torch.cuda.synchronize()
 
     s_main = torch.cuda.Stream(device=dev)
-    s_retr = torch.cuda.Stream(device=dev)
+    s_retr = s_main if args.serial else torch.cuda.Stream(device=dev)
     ws = H.workspace(H.decode_block_workspace(hd, b, B, S, k_max), dev)
     state = {"a": 0}
 
@@ -284,9 +287,11 @@ def main():
         "config": {"workload": wl.name, "batch": b, "seq_len": S, "block": B, "steps": T,
                    "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "budget_tokens": k_b,
                    "layers": 1, "mode": "dense" if args.dense else "sparse",
-                   "graph": bool(args.graph),
-                   "step": "one pipelined block: next-block selection on a second stream "
-                           "overlapped with T denoising steps, join, append, swap"},
+                   "graph": bool(args.graph), "streams": 1 if args.serial else 2,
+                   "step": ("one block on one stream: next-block selection, T denoising "
+                            "steps, append, swap" if args.serial else
+                            "one pipelined block: next-block selection on a second stream "
+                            "overlapped with T denoising steps, join, append, swap")},
         # B*G query rows per KV head give 4*B*G*d flops per 4*d bytes of bf16 K+V
         # (B*G = 128: 128 flop/B, below the 2.5 PFLOP/s / 8 TB/s ridge of 312):
         # the kernel is bound by HBM, and its MFMA rate is reported beside.
@@ -585,7 +590,7 @@ def bench_pipeline36(args):
                 od=torch.empty((b, B, Hq, d), dtype=torch.bfloat16, device=dev))
     torch.cuda.synchronize()
     s_main = torch.cuda.Stream(device=dev)
-    s_retr = torch.cuda.Stream(device=dev)
+    s_retr = s_main if args.serial else torch.cuda.Stream(device=dev)
 
     def run(dense):
         lens_h = np.full(b, S0, np.int32)
@@ -659,7 +664,7 @@ def bench_pipeline36(args):
            "config": {"workload": wl.name, "layers": L, "batch": b, "seq_len": S0, "block": B,
                       "steps": T, "budget": "5%", "dense_layers": nd,
                       "drafts": bool(args.drafts), "select_x": args.select_x,
-                      "graph": bool(args.graph),
+                      "graph": bool(args.graph), "streams": 1 if args.serial else 2,
                       "step": "one block: next-block selection of "
                       "all layers on the retrieval stream, T x L denoising steps on the main "
                       "stream, join, append, swap"},
