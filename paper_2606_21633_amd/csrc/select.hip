@@ -616,20 +616,21 @@ __global__ __launch_bounds__(256) void tail_kernel(const double *__restrict__ qb
   }
 }
 
-// Scores of V > 4 score rows per KV head. The fp64 MFMA's operands swap roles
-// against score_mfma_kernel: A holds 16 score rows (4 per block, a different
-// 4 in each block) and B holds 4 cached rows, the same in every block, so one
-// v_mfma_f64_4x4x4_4b forms 4 cached rows x 16 score rows. Lane l of A holds
-// score row 4 ((l / 4) % 4) + l % 4 at element slot l / 16; lane l of B holds
-// cached row l % 4 at slot l / 16; the result of lane l is score row
-// 4 ((l / 4) % 4) + l / 16 of cached row l % 4. The head dimension is
-// enumerated in the same permuted order on both operands. A workgroup takes
-// one group of 16 score rows (zero past V) and one chunk of 2048 cached rows;
-// its 4 waves take interleaved 16-row tiles (4 chains of 4 rows) with the
-// next tile's loads in flight. The groups of one chunk have consecutive block
-// ids, so they read the chunk at about the same time. (With 512-byte rows a
-// tile is 2 chains of 4 rows, to keep two tiles in registers.)
-template <int D, bool BF16, bool PAGED>
+// Scores of V > 4 score rows per KV head on the fp64 matrix cores. In one
+// v_mfma_f64_4x4x4_4b the four blocks hold four different groups of 4 cached
+// rows (B) against the same 4 score rows (A, the same in every block), so one
+// instruction forms 4 score rows x 16 cached rows: lane l of B holds cached
+// row l % 16 at element slot l / 16, lane l of A holds score row l % 4 at
+// slot l / 16, and the result of lane l is score row l / 16 of cached row
+// l % 16. The head dimension is enumerated in the same permuted order on both
+// operands, so a lane reads whole 16-byte pieces of its cached row. A
+// workgroup takes NQ = 4 NG score rows (zero past V; their queries staged in
+// LDS in operand order) and one chunk of 2048 cached rows; its 4 waves take
+// interleaved 16-row tiles with the next tile's loads in flight. Each cached
+// element is loaded and converted once per workgroup and feeds NG MFMAs (one
+// per group of 4 score rows). The score-row groups of one chunk have
+// consecutive block ids, so they read the chunk at about the same time.
+template <int D, bool BF16, bool PAGED, int NG>
 __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
                                                             const double *__restrict__ qx,
                                                             double *__restrict__ zspill,
@@ -642,11 +643,13 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
   constexpr int NP = D * ELT / 64;              // pieces per lane and cached row
   constexpr int NS = D / 4;                     // MFMA steps over the head dimension
   constexpr int NW = 4;                         // waves per workgroup
-  constexpr int NCH = D * ELT > 256 ? 2 : 4;    // chains of 4 cached rows per tile
-  constexpr int TR = 4 * NCH;                   // cached rows per wave tile
+  constexpr int TR = 16;                        // cached rows per wave tile
   constexpr int TPW = kScoreChunk / (TR * NW);  // tiles per wave
+  constexpr int NQ = 4 * NG;                    // score rows per workgroup
   static_assert(NP * EPP == NS, "head dimension split");
-  __shared__ double red[NW][16], red2[NW][16];
+  // queries in A-operand order: [step][slot][group][row of the group]
+  __shared__ double qs[NS * 4 * NG * 4];
+  __shared__ double red[NW][NQ], red2[NW][NQ];
 
   const int vg = blockIdx.x % nvg, chunk = blockIdx.x / nvg, h = blockIdx.y, b = blockIdx.z;
   const int64_t S = kv_len(kv, b);
@@ -654,23 +657,22 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
   if (c0 >= S) return;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t bh = (int64_t)b * Hkv + h;
-  const int kq = lane >> 4, blk = (lane >> 2) & 3, j = lane & 3;
-  const int va = vg * 16 + 4 * blk + j;    // A: score row of this lane
-  const int vz = vg * 16 + 4 * blk + kq;   // result: score row of this lane (cached row j)
+  const int kq = lane >> 4;   // element slot (A and B); score row of the result
+  const int cr = lane & 15;   // cached row of B and of the result
+  const int ia = lane & 3;    // score row of A
 
-  // A operand of every step: the score row's query at the permuted element
-  double qa[NS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const int e = (s / EPP) * (4 * EPP) + kq * EPP + s % EPP;
-    const double q = qx[(bh * D + e) * V + (va < V ? va : V - 1)];
-    qa[s] = va < V ? q : 0.0;
+  for (int t = threadIdx.x; t < NS * 4 * NG * 4; t += 256) {
+    const int i = t % 4, g = (t / 4) % NG, k = (t / (4 * NG)) % 4, st = t / (16 * NG);
+    const int e = (st / EPP) * (4 * EPP) + k * EPP + st % EPP;
+    const int v = vg * NQ + 4 * g + i;
+    qs[t] = v < V ? qx[(bh * D + e) * V + v] : 0.0;
   }
-
-  const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + kq * 16;
-  // 16-byte piece p of cached row s (the lane's slot): row-by-row page lookup
   __shared__ int32_t spt[PAGED ? kChunkPages : 1];
   if constexpr (PAGED) stage_chunk_pages(kv, b, c0, S, spt);
+  __syncthreads();
+
+  const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + kq * 16;
+  // 16-byte piece p of cached row s (the lane's slot)
   auto row_ptr = [&](int64_t s) -> const char * {
     if (PAGED) {
       const int64_t page = spt[(s >> kv.page_shift) - (c0 >> kv.page_shift)];
@@ -680,20 +682,16 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
     return kbase + s * kv.ss * ELT;
   };
   auto tile_row0 = [&](int t) { return c0 + (int64_t)(t * NW + wave) * TR; };
-  // B operand pieces of a tile: chain c holds cached row r0 + 4c + j
-  uint4 kb[2][NCH][NP];
-  auto load_tile = [&](int t, uint4 (&dst)[NCH][NP]) {
+  uint4 kb[2][NP];
+  auto load_tile = [&](int t, uint4 (&dst)[NP]) {
     const int64_t r0 = tile_row0(t);
+    const int64_t s = r0 + cr;
+    const bool ok = s < S;
+    const char *p = row_ptr(ok ? s : r0);
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int64_t s = r0 + 4 * c + j;
-      const bool ok = s < S;
-      const char *p = row_ptr(ok ? s : r0);
-#pragma unroll
-      for (int q = 0; q < NP; ++q) {
-        dst[c][q] = make_uint4(0u, 0u, 0u, 0u);
-        if (ok) dst[c][q] = ldg16_nt(p + q * 64);
-      }
+    for (int q = 0; q < NP; ++q) {
+      dst[q] = make_uint4(0u, 0u, 0u, 0u);
+      if (ok) dst[q] = ldg16_nt(p + q * 64);
     }
   };
   auto elem = [&](const uint4 *pc, int s) -> double {
@@ -704,30 +702,39 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
     return (double)__uint_as_float(w[e]);
   };
 
-  double m_l = -INFINITY, l_l = 0.0;
-  auto step = [&](int t, uint4 (&cur)[NCH][NP], uint4 (&nxt)[NCH][NP]) -> bool {
+  double m_l[NG], l_l[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) { m_l[g] = -INFINITY; l_l[g] = 0.0; }
+  const double *qa = qs + kq * (4 * NG) + ia;
+  auto step = [&](int t, uint4 (&cur)[NP], uint4 (&nxt)[NP]) -> bool {
     const int64_t r0 = tile_row0(t);
     if (r0 >= S) return false;  // uniform: later tiles of this wave start later still
     if (t + 1 < TPW && tile_row0(t + 1) < S) load_tile(t + 1, nxt);
-    double acc[NCH];
+    double acc[NG];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) acc[c] = 0.0;
+    for (int g = 0; g < NG; ++g) acc[g] = 0.0;
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
+    for (int st = 0; st < NS; ++st) {
+      const double bk = elem(cur, st);
 #pragma unroll
-      for (int c = 0; c < NCH; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f64_4x4x4f64(qa[s], elem(cur[c], s), acc[c], 0, 0, 0);
+      for (int g = 0; g < NG; ++g)
+        acc[g] = __builtin_amdgcn_mfma_f64_4x4x4f64(qa[st * (16 * NG) + 4 * g], bk, acc[g], 0,
+                                                    0, 0);
+    }
+    const int64_t s = r0 + cr;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int64_t s = r0 + 4 * c + j;
-      if (vz < V && s < S) {
-        const double z = acc[c] * scale;
-        zspill[(bh * S_pad + s) * V + vz] = z;
-        const double dz = z - m_l;
+    for (int g = 0; g < NG; ++g) {
+      const int v = vg * NQ + 4 * g + kq;
+      if (v < V && s < S) {
+        const double z = acc[g] * scale;
+        zspill[(bh * S_pad + s) * V + v] = z;
+        // one exp per score: exp(-|z - m|) either rescales the old sum or is
+        // the new term
+        const double dz = z - m_l[g];
         const double e = exp(-fabs(dz));
         const bool up = dz > 0.0;
-        l_l = up ? fma(l_l, e, 1.0) : l_l + e;
-        m_l = up ? z : m_l;
+        l_l[g] = up ? fma(l_l[g], e, 1.0) : l_l[g] + e;
+        m_l[g] = up ? z : m_l[g];
       }
     }
     return true;
@@ -739,30 +746,41 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
     if (!step(t + 1, kb[1], kb[0])) break;
   }
 
-  // chunk statistics of each score row: over its 4 cached-row lanes, then the waves
-  double m = m_l;
-  m = fmax(m, __shfl_xor(m, 1, 64));
-  m = fmax(m, __shfl_xor(m, 2, 64));
-  const int slot = 4 * blk + kq;  // score row within the group
-  if (j == 0) red[wave][slot] = m;
+  // chunk statistics of each score row: over its 16 cached-row lanes, then the
+  // waves, in a fixed order
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    double m = m_l[g];
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) m = fmax(m, __shfl_xor(m, off, 64));
+    if (cr == 0) red[wave][4 * g + kq] = m;
+  }
   __syncthreads();
-  const double mc = fmax(fmax(red[0][slot], red[1][slot]), fmax(red[2][slot], red[3][slot]));
-  double v = m_l == -INFINITY ? 0.0 : l_l * exp(m_l - mc);
-  v += __shfl_xor(v, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  if (j == 0) red2[wave][slot] = v;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int slot = 4 * g + kq;
+    const double mc = fmax(fmax(red[0][slot], red[1][slot]), fmax(red[2][slot], red[3][slot]));
+    double v = m_l[g] == -INFINITY ? 0.0 : l_l[g] * exp(m_l[g] - mc);
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 64);
+    if (cr == 0) red2[wave][slot] = v;
+  }
   __syncthreads();
-  if (wave == 0 && j == 0 && vz < V) {
-    double *p = part + ((bh * nslot + chunk) * V + vz) * 2;
+  for (int slot = threadIdx.x; slot < NQ; slot += 256) {
+    const int v = vg * NQ + slot;
+    if (v >= V) continue;
+    const double mc = fmax(fmax(red[0][slot], red[1][slot]), fmax(red[2][slot], red[3][slot]));
+    double *p = part + ((bh * nslot + chunk) * V + v) * 2;
     p[0] = mc;
     p[1] = ((red2[0][slot] + red2[1][slot]) + red2[2][slot]) + red2[3][slot];
   }
 }
 
 // GQA importance for any number V of score rows per KV head: as norm_kernel,
-// with the statistics in LDS and LPR lanes per cached row (a power of two,
-// up to 64) summing the V terms, combined by a butterfly of shuffles (every
-// lane of the row ends with the same sum, so equal score rows give equal keys).
+// with the statistics in LDS and LPR lanes per cached row (the power of two
+// that gives each lane at most 8 of the V terms, up to 64 lanes) summing the
+// terms, combined by a butterfly of shuffles (every lane of the row ends with
+// the same sum, so equal score rows give equal keys).
 __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restrict__ lens,
                                                         const double *__restrict__ zspill,
                                                         const double *__restrict__ part,
@@ -790,7 +808,7 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
   __syncthreads();
 
   int lpr = 1;
-  while (lpr < V && lpr < 64) lpr <<= 1;
+  while (lpr * 8 < V && lpr < 64) lpr <<= 1;
   const int rpi = 64 / lpr;                 // cached rows per wave and round
   const int sub = lane / lpr, q = lane % lpr;
   const int64_t c1 = min(c0 + (int64_t)kScoreChunk, S);
@@ -800,7 +818,17 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
     double acc = 0.0;
     if (valid) {
       const double *zz = zspill + (bh * S_pad + s) * V;
-      for (int v = q; v < V; v += lpr) acc += exp(zz[v] - sm[v]) * sinv[v];
+      for (int v0 = q; v0 < V; v0 += 8 * lpr) {
+        // up to 8 terms of this lane, every load issued before the exps
+        double z[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) z[u] = v0 + u * lpr < V ? zz[v0 + u * lpr] : 0.0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int v = v0 + u * lpr;
+          if (v < V) acc += exp(z[u] - sm[v]) * sinv[v];
+        }
+      }
     }
     for (int off = lpr >> 1; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
     const bool lead = valid && q == 0;
@@ -1309,14 +1337,21 @@ hipError_t launch_select_xq_t(int batch, int block, int x, const void *q_sel,
   else if (V == 2) launch_score_norm_small<D, 2, BF16>(kv, batch, Hkv, ws, nslot, scale, stream);
   else if (V == 4) launch_score_norm_small<D, 4, BF16>(kv, batch, Hkv, ws, nslot, scale, stream);
   else {
-    const int nvg = (V + 15) / 16;
+    // groups of 4 score rows per workgroup: the fewest that cover V, at most 16
+    const int ng = V <= 8 ? 2 : V <= 16 ? 4 : V <= 32 ? 8 : 16;
+    const int nvg = (V + 4 * ng - 1) / (4 * ng);
     const dim3 grid_s(ws.nchunk * nvg, Hkv, batch);
-    if (kv.pt)
-      score_rows_kernel<D, BF16, true><<<grid_s, 256, 0, stream>>>(
-          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, nslot, scale);
-    else
-      score_rows_kernel<D, BF16, false><<<grid_s, 256, 0, stream>>>(
-          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, nslot, scale);
+#define HERALD_SCORE_ROWS(NG_)                                                                 \
+  if (ng == NG_) {                                                                             \
+    if (kv.pt)                                                                                 \
+      score_rows_kernel<D, BF16, true, NG_><<<grid_s, 256, 0, stream>>>(                       \
+          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, nslot, scale);               \
+    else                                                                                       \
+      score_rows_kernel<D, BF16, false, NG_><<<grid_s, 256, 0, stream>>>(                      \
+          kv, ws.qbar, ws.espill, ws.part, Hkv, V, nvg, ws.S_pad, nslot, scale);               \
+  }
+    HERALD_SCORE_ROWS(2) HERALD_SCORE_ROWS(4) HERALD_SCORE_ROWS(8) HERALD_SCORE_ROWS(16)
+#undef HERALD_SCORE_ROWS
     norm_rows_kernel<<<dim3(ws.nchunk, Hkv, batch), 256, 0, stream>>>(
         kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv, V, ws.S_pad, nslot, kv.max_len);
   }
