@@ -590,15 +590,10 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   }
 }
 
-// Workgroups the split-KV plan aims for; read once per process.
-int target_wgs() {
-  static const int t = [] {
-    const char *v = getenv("HERALD_ATTN_TARGET_WGS");
-    const int x = v ? atoi(v) : 256;
-    return x > 0 ? x : 256;
-  }();
-  return t;
-}
+// Workgroups the split-KV plan aims for: one per CU of the 256-CU gfx950
+// (each workgroup takes a whole CU's registers). The plan is host-only (the
+// workspace queries run without a device), so this is not read from the GPU.
+constexpr int kTargetWgs = 256;
 
 }  // namespace
 
@@ -629,7 +624,7 @@ AttnPlan attn_plan(const herald_heads &hd, int batch, int block, int64_t max_ctx
   const int64_t ntile = (max_keys + p.key_tile - 1) / p.key_tile;
   const int64_t base = (int64_t)batch * hd.num_kv_heads * p.n_mblk;
   // one workgroup per CU; every split gets at least one tile per pipeline
-  int64_t want = (target_wgs() + base - 1) / base;
+  int64_t want = (kTargetWgs + base - 1) / base;
   if (want < 1) want = 1;
   const int64_t most = (ntile + p.pipes - 1) / p.pipes;
   const int64_t ns = want < most ? want : most;
