@@ -700,11 +700,36 @@ def cpu_baseline(wl, inp, k_b, nseq, nsteps, dense):
         t_sel += t1 - t0
         t_att += t2 - t1
     block_s = (t_sel / nseq + t_att / (nseq * nsteps) * wl.steps) * wl.batch
-    return {"value": round(wl.steps / block_s, 6), "unit": "steps/s",
-            "cores": oracle.threads(), "kind": "oracle",
-            "sample": f"{nseq} of {wl.batch} sequences x (selection+gather and {nsteps} of "
-                      f"{wl.steps} attention steps), scaled to one block of the batch",
-            "seconds": round(t_sel + t_att, 2)}
+    res = {"value": round(wl.steps / block_s, 6), "unit": "steps/s",
+           "cores": oracle.threads(), "kind": "oracle",
+           "sample": f"{nseq} of {wl.batch} sequences x (selection+gather and {nsteps} of "
+                     f"{wl.steps} attention steps), scaled to one block of the batch",
+           "seconds": round(t_sel + t_att, 2)}
+    # the same oracle on one core: one sequence, its selection + gather and eight
+    # attention steps, scaled the same way
+    n_all = oracle.threads()
+    oracle.set_threads(1)
+    try:
+        K, V = inp["k"][0, :, :S], inp["v"][0, :, :S]
+        t0 = time.perf_counter()
+        if dense:
+            pk, pv = K, V
+        else:
+            idx, _, _, _ = oracle.select(inp["q_next"][0], K, k_b)
+            pk, pv = oracle.gather(K, idx), oracle.gather(V, idx)
+        t1 = time.perf_counter()
+        n1 = min(8, wl.steps)
+        for t in range(n1):
+            oracle.attn(inp["q"][t][0], pk, pv, inp["blk_k"][t][0], inp["blk_v"][t][0])
+        t2 = time.perf_counter()
+    finally:
+        oracle.set_threads(n_all)
+    block1 = ((t1 - t0) + (t2 - t1) / n1 * wl.steps) * wl.batch
+    res["single_core"] = {"value": round(wl.steps / block1, 6), "unit": "steps/s", "cores": 1,
+                          "sample": f"1 of {wl.batch} sequences x (selection+gather and {n1} "
+                                    f"of {wl.steps} attention steps), scaled to one block of "
+                                    f"the batch", "seconds": round(t2 - t0, 2)}
+    return res
 
 
 if __name__ == "__main__":

@@ -77,6 +77,8 @@ def _load():
     i64, i32, p, d = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_double
     lib.herald_oracle_threads.restype = i32
     lib.herald_oracle_threads.argtypes = []
+    lib.herald_oracle_set_threads.restype = None
+    lib.herald_oracle_set_threads.argtypes = [i32]
     lib.herald_oracle_budget.restype = i64
     lib.herald_oracle_budget.argtypes = [i64, i64, i64]
     lib.herald_oracle_select.restype = i32
@@ -125,6 +127,11 @@ def _ptr(a):
 def threads() -> int:
     """OpenMP threads the oracle's loops use."""
     return int(_load().herald_oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Sets the OpenMP threads of the oracle's loops (at least 1)."""
+    _load().herald_oracle_set_threads(int(n))
 
 
 def budget(S: int, num: int = 1, den: int = 20) -> int:

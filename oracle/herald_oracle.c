@@ -80,6 +80,9 @@ static size_t elem_size(int type) {
 /* Threads the OpenMP loops below run on. */
 int herald_oracle_threads(void) { return omp_get_max_threads(); }
 
+/* Sets the threads of the OpenMP loops (n >= 1), e.g. 1 to time one core. */
+void herald_oracle_set_threads(int n) { omp_set_num_threads(n < 1 ? 1 : n); }
+
 int64_t herald_oracle_budget(int64_t S, int64_t num, int64_t den) {
   /* k = clamp(floor(S*num/den + 1/2), 1, S) evaluated exactly in integers */
   if (S <= 0 || den <= 0 || num < 0) return 0;
