@@ -75,8 +75,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the hot path is measured on a single "
-              "MI355X and this build has no multi-GPU path (see DESIGN.md, sharding).",
-              file=sys.stderr)
+              "MI355X, and the library has no multi-GPU path (each GPU would take its own "
+              "sequences or KV heads with no exchange).", file=sys.stderr)
         sys.exit(2)
 
     import torch
