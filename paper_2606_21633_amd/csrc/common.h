@@ -93,6 +93,12 @@ struct SelectWs {
   uint64_t *keys;   // [b][Hkv][S_pad]
   uint32_t *hist;   // [b][Hkv][2048]
   float *opart;     // [b][Hkv][nchunk + 1][G][d]: attention output parts (optional output)
+  uint64_t *cut;    // [b][Hkv][4]: the top-k cut (boundary prefix, its shift, keys of
+                    // the boundary bucket still to take, whole-bucket flag and k)
+  uint32_t *ecnt;   // [b][Hkv][nchunk]: keys above the cut (high 16 bits) and in the
+                    // boundary bucket (low 16 bits) per chunk
+  uint8_t *emark;   // [b][Hkv][nchunk][2][256]: per 8 consecutive keys, bit masks of
+                    // the keys above the cut and of those in the boundary bucket
   int64_t S_pad;
   int nchunk;
 };

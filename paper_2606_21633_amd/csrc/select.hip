@@ -36,7 +36,6 @@ namespace {
 
 constexpr int kTopkThreads = 1024;
 constexpr int kCandCap = 16384;  // LDS candidates (128 KiB of keys)
-constexpr int kEmitPerThread = 16;  // consecutive keys per thread in the emission
 constexpr int kKeysPerThread = 16;  // keys per thread and round in the passes over S
 
 // (m, l) <- softmax-statistics merge of (m, l) and (m2, l2).
@@ -1083,7 +1082,8 @@ __device__ __forceinline__ void find_digit(const uint32_t *cnt, int nbins, int r
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     const int32_t *__restrict__ lens, const int32_t *__restrict__ kps, int k_max,
     const uint64_t *__restrict__ keys, const uint32_t *__restrict__ hist,
-    int32_t *__restrict__ idx_out, int Hkv, int64_t S_pad, int64_t max_len) {
+    int32_t *__restrict__ idx_out, uint64_t *__restrict__ cut, int Hkv, int64_t S_pad,
+    int64_t max_len) {
   constexpr int KPT = kKeysPerThread;
   __shared__ uint32_t cnt[kHistBins];
   __shared__ uint64_t cand[kCandCap];
@@ -1101,6 +1101,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
 
   if (k == 0 || k == S) {
     for (int j = tid; j < k_max; j += kTopkThreads) out[j] = j < k ? j : -1;
+    if (tid == 0) cut[bh * 4 + 3] = 0;  // nothing left for the emission kernels
     return;
   }
 
@@ -1186,60 +1187,157 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     if (!in_lds && c != r && c <= kCandCap) compact();
   }
 
-  // Ordered emission: keys above the boundary bucket always; bucket members
-  // (equal top bits; exact ties once L == 0) all of them when the bucket holds
-  // exactly r keys, else the r of lowest index. Each thread takes E
-  // consecutive indices, so a block scan of the per-thread counts gives the
-  // output positions in ascending index order.
-  constexpr int E = kEmitPerThread;
-  const bool whole_bucket = c == r;
-  int base_eq = 0, base_sel = 0;
-  for (int64_t t0 = 0; t0 < S; t0 += (int64_t)kTopkThreads * E) {
-    const int64_t s0 = t0 + (int64_t)tid * E;
-    uint64_t key[E];
-    if (s0 + E <= S) {
-#pragma unroll
-      for (int j = 0; j < E / 2; ++j) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(kb + s0 + 2 * j);
-        key[2 * j] = (uint64_t)v.x | ((uint64_t)v.y << 32);
-        key[2 * j + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < E; ++u) key[u] = s0 + u < S ? kb[s0 + u] : 0;
-    }
-    uint32_t gt = 0, eq = 0;
-#pragma unroll
-    for (int u = 0; u < E; ++u) {
-      const bool valid = s0 + u < S;
-      const uint64_t hi = valid ? (key[u] >> L) : 0;
-      gt |= (uint32_t)(valid && hi > P) << u;
-      eq |= (uint32_t)(valid && hi == P) << u;
-    }
-    uint32_t take = gt | eq;
-    if (!whole_bucket) {
-      int tot_eq;
-      int rank = base_eq + block_excl_scan(__popc(eq), wsum, &tot_eq);
-      take = gt;
-#pragma unroll
-      for (int u = 0; u < E; ++u)
-        if ((eq >> u) & 1u) {
-          if (rank < r) take |= 1u << u;
-          ++rank;
-        }
-      base_eq += tot_eq;
-    }
-    int tot_take;
-    int pos = base_sel + block_excl_scan(__popc(take), wsum, &tot_take);
-#pragma unroll
-    for (int u = 0; u < E; ++u)
-      if ((take >> u) & 1u) {
-        if (pos < k) out[pos] = (int32_t)(s0 + u);  // counts are exact; guard anyway
-        ++pos;
-      }
-    base_sel += tot_take;
+  // The cut, for the ordered emission of emit_count_kernel and
+  // emit_write_kernel: keys whose top (64 - L) bits exceed P are taken; keys
+  // of the boundary bucket (top bits equal to P; exact ties once L == 0) all
+  // of them when the bucket holds exactly r keys, else the r of lowest index.
+  if (tid == 0) {
+    cut[bh * 4 + 0] = P;
+    cut[bh * 4 + 1] = (uint64_t)L;
+    cut[bh * 4 + 2] = (uint64_t)r;
+    cut[bh * 4 + 3] = (uint64_t)(c == r ? 2 : 1);  // 2: whole bucket, 1: r lowest
   }
   for (int j = k + tid; j < k_max; j += kTopkThreads) out[j] = -1;
+}
+
+// Ordered emission of the top-k, one workgroup per chunk of 2048 keys of a
+// (KV head, sequence): emit_count_kernel marks and counts the chunk's keys
+// above the cut and in the boundary bucket (one byte of each mask per 8
+// consecutive keys); emit_write_kernel adds up the counts of the chunks
+// before its own, and each thread, owning 8 consecutive keys, finds its
+// output positions from the marks with one block scan, so the indices come
+// out in ascending order.
+__device__ __forceinline__ void chunk_marks(const uint64_t *kb, int64_t s0, int64_t S,
+                                            uint64_t P, int L, uint32_t &gt, uint32_t &eq) {
+  uint64_t key[8];
+  if (s0 + 8 <= S) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(kb + s0 + 2 * j);
+      key[2 * j] = (uint64_t)v.x | ((uint64_t)v.y << 32);
+      key[2 * j + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) key[u] = s0 + u < S ? kb[s0 + u] : 0;
+  }
+  gt = eq = 0;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const bool valid = s0 + u < S;
+    // (L == 64 never happens: the first digit already fixes 12 bits)
+    const uint64_t hi = valid ? (key[u] >> L) : 0;
+    gt |= (uint32_t)(valid && hi > P) << u;
+    eq |= (uint32_t)(valid && hi == P) << u;
+  }
+}
+
+__global__ __launch_bounds__(256) void emit_count_kernel(
+    const int32_t *__restrict__ lens, const uint64_t *__restrict__ keys,
+    const uint64_t *__restrict__ cut, uint32_t *__restrict__ ecnt, uint8_t *__restrict__ emark,
+    int Hkv, int64_t S_pad, int nchunk, int64_t max_len) {
+  __shared__ uint32_t wsum[4];
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  if (c0 >= S || cut[bh * 4 + 3] == 0) return;
+  uint32_t gt, eq;
+  chunk_marks(keys + bh * S_pad, c0 + threadIdx.x * 8, S, cut[bh * 4], (int)cut[bh * 4 + 1],
+              gt, eq);
+  uint8_t *mk = emark + (bh * nchunk + chunk) * 512;
+  mk[threadIdx.x] = (uint8_t)gt;
+  mk[256 + threadIdx.x] = (uint8_t)eq;
+  uint32_t v = ((uint32_t)__popc(gt) << 16) | (uint32_t)__popc(eq);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) ecnt[bh * nchunk + chunk] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
+__global__ __launch_bounds__(256) void emit_write_kernel(
+    const int32_t *__restrict__ lens, const int32_t *__restrict__ kps, int k_max,
+    const uint64_t *__restrict__ cut, const uint32_t *__restrict__ ecnt,
+    const uint8_t *__restrict__ emark, int32_t *__restrict__ idx_out, int Hkv, int nchunk,
+    int64_t max_len) {
+  __shared__ uint32_t wsum[4], wbase[4];
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int64_t bh = (int64_t)b * Hkv + h;
+  const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
+  const int64_t c0 = (int64_t)chunk * kScoreChunk;
+  const uint64_t mode = cut[bh * 4 + 3];
+  if (c0 >= S || mode == 0) return;
+  const int k = clamp_k(kps[b], S, k_max);
+  const int r = (int)cut[bh * 4 + 2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // keys above the cut and in the bucket in the chunks before this one (each
+  // count below 2^16: a chunk holds 2048 keys)
+  uint32_t gt_before = 0, eq_before = 0;
+  for (int c = tid; c < chunk; c += 256) {
+    const uint32_t v = ecnt[bh * nchunk + c];
+    gt_before += v >> 16;
+    eq_before += v & 0xffffu;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    gt_before += __shfl_xor(gt_before, off, 64);
+    eq_before += __shfl_xor(eq_before, off, 64);
+  }
+  if (lane == 0) { wsum[wave] = gt_before; wbase[wave] = eq_before; }
+  __syncthreads();
+  gt_before = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+  eq_before = ((wbase[0] + wbase[1]) + wbase[2]) + wbase[3];
+  __syncthreads();
+
+  const int64_t s0 = c0 + tid * 8;
+  const uint8_t *mk = emark + (bh * nchunk + chunk) * 512;
+  const uint32_t gt = mk[tid], eq = mk[256 + tid];
+  // exclusive scan over the threads of (keys above, bucket keys), packed
+  const uint32_t mine = ((uint32_t)__popc(gt) << 16) | (uint32_t)__popc(eq);
+  uint32_t incl = mine;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  uint32_t excl = incl - mine;
+  for (int w = 0; w < wave; ++w) excl += wsum[w];
+  // bucket keys before this thread's, over the whole sequence, and how many
+  // of them are taken; then this thread's first output position
+  const int eq_rank = (int)(eq_before + (excl & 0xffffu));
+  const bool whole = mode == 2;
+  auto taken_eq = [&](int n) { return whole ? n : max(0, min(n, r)); };
+  int pos = (int)(gt_before + (excl >> 16)) + taken_eq(eq_rank);
+  int rank = eq_rank;
+  int32_t *out = idx_out + bh * k_max;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    bool take = (gt >> u) & 1u;
+    if ((eq >> u) & 1u) {
+      take = whole || rank < r;
+      ++rank;
+    }
+    if (take) {
+      if (pos < k) out[pos] = (int32_t)(s0 + u);  // counts are exact; guard anyway
+      ++pos;
+    }
+  }
+}
+
+// Top-k of every (KV head, sequence) from the keys and the first-level
+// histogram: the cut, then the chunk-parallel ordered emission.
+void launch_topk(const KvView &kv, int batch, int Hkv, const int32_t *k_per_seq, int k_max,
+                 int32_t *idx_out, const SelectWs &ws, hipStream_t stream) {
+  topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
+      kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, ws.cut, Hkv, ws.S_pad, kv.max_len);
+  const dim3 grid(ws.nchunk, Hkv, batch);
+  emit_count_kernel<<<grid, 256, 0, stream>>>(kv.lens, ws.keys, ws.cut, ws.ecnt, ws.emark, Hkv,
+                                              ws.S_pad, ws.nchunk, kv.max_len);
+  emit_write_kernel<<<grid, 256, 0, stream>>>(kv.lens, k_per_seq, k_max, ws.cut, ws.ecnt,
+                                              ws.emark, idx_out, Hkv, ws.nchunk, kv.max_len);
 }
 
 // The optional attention output (after norm has written the keys: the
@@ -1296,8 +1394,7 @@ hipError_t launch_select_t(int batch, int block, const void *q_sel, const KvView
   }
   norm_kernel<G><<<grid, 256, 0, stream>>>(kv.lens, ws.espill, ws.part, ws.keys, ws.hist,
                                            Hkv, ws.S_pad, nslot, kv.max_len);
-  topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
-      kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
+  launch_topk(kv, batch, Hkv, k_per_seq, k_max, idx_out, ws, stream);
   if (o_out)
     launch_out<D, BF16>(kv, batch, Hq, Hkv, G, tail, tail_v, n_tail, o_out, ws, nslot, scale,
                         stream);
@@ -1355,8 +1452,7 @@ hipError_t launch_select_xq_t(int batch, int block, int x, const void *q_sel,
     norm_rows_kernel<<<dim3(ws.nchunk, Hkv, batch), 256, 0, stream>>>(
         kv.lens, ws.espill, ws.part, ws.keys, ws.hist, Hkv, V, ws.S_pad, nslot, kv.max_len);
   }
-  topk_kernel<<<dim3(Hkv, batch), kTopkThreads, 0, stream>>>(
-      kv.lens, k_per_seq, k_max, ws.keys, ws.hist, idx_out, Hkv, ws.S_pad, kv.max_len);
+  launch_topk(kv, batch, Hkv, k_per_seq, k_max, idx_out, ws, stream);
   if (o_out)
     launch_out<D, BF16>(kv, batch, Hq, Hkv, V, tail, tail_v, n_tail, o_out, ws, nslot, scale,
                         stream);
@@ -1380,6 +1476,9 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
   const size_t o_keys = off; off = align256(off + bh * S_pad * sizeof(uint64_t));
   const size_t o_hist = off; off = align256(off + bh * kHistBins * sizeof(uint32_t));
   const size_t o_opart = off; off = align256(off + bh * (nchunk + 1) * G * d * sizeof(float));
+  const size_t o_cut = off;  off = align256(off + bh * 4 * sizeof(uint64_t));
+  const size_t o_ecnt = off; off = align256(off + bh * nchunk * sizeof(uint32_t));
+  const size_t o_emark = off; off = align256(off + bh * nchunk * 2 * 256);
   if (layout) {
     layout->qbar = reinterpret_cast<double *>(base + o_qbar);
     layout->espill = reinterpret_cast<double *>(base + o_z);
@@ -1387,6 +1486,9 @@ size_t select_ws_bytes(int batch, int Hq, int Hkv, int d, int64_t max_seq_len,
     layout->keys = reinterpret_cast<uint64_t *>(base + o_keys);
     layout->hist = reinterpret_cast<uint32_t *>(base + o_hist);
     layout->opart = reinterpret_cast<float *>(base + o_opart);
+    layout->cut = reinterpret_cast<uint64_t *>(base + o_cut);
+    layout->ecnt = reinterpret_cast<uint32_t *>(base + o_ecnt);
+    layout->emark = reinterpret_cast<uint8_t *>(base + o_emark);
     layout->S_pad = S_pad;
     layout->nchunk = nchunk;
   }
