@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include "common.h"
+#include "select.h"
 
 using namespace herald;
 

@@ -30,6 +30,7 @@
 #include <math.h>
 
 #include "common.h"
+#include "select.h"
 
 namespace herald {
 namespace {
