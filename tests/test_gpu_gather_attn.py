@@ -109,6 +109,13 @@ def test_attn_bf16_layer_32k_pool_shape():
     run_attn("bf16", 16, 32, 8, 128, 32, [1638] * 16, seed=9, seqs=[0, 5, 10, 15])
 
 
+def test_attn_bf16_long_128k_pool_shape():
+    """The denoising step of the 128K-context layer: 4 sequences, 6554 pool
+    rows + 32 block rows per KV head, keys split 4 ways and combined; two
+    sequences checked by the oracle."""
+    run_attn("bf16", 4, 32, 8, 128, 32, [6554] * 4, seed=13, seqs=[0, 3])
+
+
 def test_attn_bf16_dense_over_full_cache_shape():
     """Dense attention (the 100%-budget baseline) over 65536 cached rows."""
     run_attn("bf16", 2, 32, 8, 128, 32, [65536, 40000], seed=10)
