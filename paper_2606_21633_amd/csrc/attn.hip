@@ -392,7 +392,7 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
   // (it + 1) & 1, tile it + 3 is fetched into that set, tile it is consumed
   // from stage it & 1. The loop is unrolled by two so that the register sets
   // are named statically.
-  // The two waves that share a SIMD belong to pipelines p and p + 2; the
+  // The two waves that share a SIMD belong to pipelines p and p + P / 2; the
   // first half of the pipelines computes before it stashes and fetches, the
   // second half after, so that one wave's MFMA work meets the other's memory
   // and VALU work instead of the same unit.
@@ -611,7 +611,6 @@ AttnPlan attn_plan(const herald_heads &hd, int batch, int block, int64_t max_ctx
   }
   // Row blocks of 64 rows: 4 pipelines of 2 waves x 32 rows (512 threads);
   // blocks of at most 32 rows: 4 pipelines of one wave.
-  p.pipes = 4;
   p.stages = 2;
   p.key_tile = 32;
   if (p.M > 32) {
@@ -619,21 +618,31 @@ AttnPlan attn_plan(const herald_heads &hd, int batch, int block, int64_t max_ctx
   } else {
     p.rows_per_wave = p.M > 16 ? 32 : 16, p.nwaves = 1;
   }
-  p.n_mblk = (p.M + p.rows_per_wave * p.nwaves - 1) / (p.rows_per_wave * p.nwaves);
   const int64_t max_keys = max_ctx + block;
   const int64_t ntile = (max_keys + p.key_tile - 1) / p.key_tile;
-  const int64_t base = (int64_t)batch * hd.num_kv_heads * p.n_mblk;
-  // one workgroup per CU; every split gets at least one tile per pipeline
-  int64_t want = (kTargetWgs + base - 1) / base;
-  if (want < 1) want = 1;
-  const int64_t most = (ntile + p.pipes - 1) / p.pipes;
-  const int64_t ns = want < most ? want : most;
-  const int64_t tiles_per = (ntile + ns - 1) / ns;
-  p.keys_per_split = (int)(tiles_per * p.key_tile);
-  p.nsplit = (int)((max_keys + p.keys_per_split - 1) / p.keys_per_split);
-  // nsplit <= min(want, ceil(ntile / pipes)), which grows with the context:
-  // sizing the partials by it covers every shorter context too
-  p.nsplit_cap = (int)ns;
+  auto split_keys = [&](int pipes, int nwaves) {
+    p.pipes = pipes;
+    p.nwaves = nwaves;
+    p.n_mblk = (p.M + p.rows_per_wave * p.nwaves - 1) / (p.rows_per_wave * p.nwaves);
+    const int64_t base = (int64_t)batch * hd.num_kv_heads * p.n_mblk;
+    // one workgroup per CU; every split gets at least one tile per pipeline
+    int64_t want = (kTargetWgs + base - 1) / base;
+    if (want < 1) want = 1;
+    const int64_t most = (ntile + p.pipes - 1) / p.pipes;
+    const int64_t ns = want < most ? want : most;
+    const int64_t tiles_per = (ntile + ns - 1) / ns;
+    p.keys_per_split = (int)(tiles_per * p.key_tile);
+    p.nsplit = (int)((max_keys + p.keys_per_split - 1) / p.keys_per_split);
+    // nsplit <= min(want, ceil(ntile / pipes)), which grows with the context:
+    // sizing the partials by it covers every shorter context too
+    p.nsplit_cap = (int)ns;
+  };
+  split_keys(4, p.nwaves);
+  // When the keys are split anyway (and a combine runs), 128-row blocks (2
+  // pipelines of 4 waves) read each KV head's keys once per split instead of
+  // once per 64-row block. (A shorter context under the same shapes splits
+  // at most as many ways, so partials sized by the longest one still fit.)
+  if (p.M >= 128 && p.nsplit_cap > 1) split_keys(2, 4);
   if (p.nsplit_cap > 1) {
     const size_t parts = (size_t)batch * hd.num_kv_heads * p.nsplit_cap * p.M;
     p.part_o_bytes = parts * hd.head_dim * sizeof(float);
@@ -675,22 +684,27 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, int g
   const uint16_t *bk = (const uint16_t *)blk_k, *bv = (const uint16_t *)blk_v;
   uint16_t *oo = (uint16_t *)out;
   const bool paged = ctx.pt != nullptr;
-#define HERALD_ATTN(D_, RW_, NW_, PG_)                                                   \
-  if (D == D_ && p.rows_per_wave == RW_ && p.nwaves == NW_ && paged == PG_) {            \
-    auto kfn = attn_bf16_kernel<D_, RW_, NW_, 4, PG_>;                                    \
-    constexpr int kSmem = attn_smem_bytes<D_, RW_, NW_, 4>();                             \
+#define HERALD_ATTN(D_, RW_, NW_, P_, PG_)                                               \
+  if (D == D_ && p.rows_per_wave == RW_ && p.nwaves == NW_ && p.pipes == P_ &&            \
+      paged == PG_) {                                                                    \
+    auto kfn = attn_bf16_kernel<D_, RW_, NW_, P_, PG_>;                                   \
+    constexpr int kSmem = attn_smem_bytes<D_, RW_, NW_, P_>();                            \
     static const hipError_t attr_err = hipFuncSetAttribute(                               \
         reinterpret_cast<const void *>(kfn), hipFuncAttributeMaxDynamicSharedMemorySize,  \
         kSmem);                                                                          \
     if (attr_err != hipSuccess) return attr_err;                                         \
-    kfn<<<grid, NW_ * 4 * 64, kSmem, stream>>>(qq, ctx, bk, bv, oo, part_o, part_ml,      \
+    kfn<<<grid, NW_ * P_ * 64, kSmem, stream>>>(qq, ctx, bk, bv, oo, part_o, part_ml,     \
                                                block, Hq, Hkv, G, p.M, p.n_mblk,         \
                                                p.nsplit, p.keys_per_split, sl2, groups); \
   } else
-  HERALD_ATTN(64, 32, 2, false) HERALD_ATTN(64, 32, 1, false) HERALD_ATTN(64, 16, 1, false)
-  HERALD_ATTN(128, 32, 2, false) HERALD_ATTN(128, 32, 1, false) HERALD_ATTN(128, 16, 1, false)
-  HERALD_ATTN(64, 32, 2, true) HERALD_ATTN(64, 32, 1, true) HERALD_ATTN(64, 16, 1, true)
-  HERALD_ATTN(128, 32, 2, true) HERALD_ATTN(128, 32, 1, true) HERALD_ATTN(128, 16, 1, true)
+  HERALD_ATTN(64, 32, 2, 4, false) HERALD_ATTN(64, 32, 1, 4, false)
+  HERALD_ATTN(64, 16, 1, 4, false) HERALD_ATTN(64, 32, 4, 2, false)
+  HERALD_ATTN(128, 32, 2, 4, false) HERALD_ATTN(128, 32, 1, 4, false)
+  HERALD_ATTN(128, 16, 1, 4, false) HERALD_ATTN(128, 32, 4, 2, false)
+  HERALD_ATTN(64, 32, 2, 4, true) HERALD_ATTN(64, 32, 1, 4, true)
+  HERALD_ATTN(64, 16, 1, 4, true) HERALD_ATTN(64, 32, 4, 2, true)
+  HERALD_ATTN(128, 32, 2, 4, true) HERALD_ATTN(128, 32, 1, 4, true)
+  HERALD_ATTN(128, 16, 1, 4, true) HERALD_ATTN(128, 32, 4, 2, true)
   return hipErrorInvalidValue;
 #undef HERALD_ATTN
   if (p.nsplit > 1) {
