@@ -250,8 +250,8 @@ size_t herald_block_attn_workspace(const herald_heads *heads, int32_t batch,
  * h followed by the block's own rows blk_k[b][0..block)[h]; with
  * p = softmax(q . key / sqrt(d)), out[b][i][hq] = sum_j p_j value_j. No mask.
  *   q            device [batch][block][H_q][d]
- *   ctx          the sparse pool (or the full cache for dense attention);
- *                contiguous views only; max_seq_len bounds the rows used.
+ *   ctx          the sparse pool (or the full cache for dense attention),
+ *                contiguous or paged; max_seq_len bounds the rows used.
  *   blk_k, blk_v device [batch][block][H_kv][d]
  *   out          device [batch][block][H_q][d] in heads->dtype
  * bf16 inputs run on bf16 MFMA with fp32 accumulation and softmax; the output

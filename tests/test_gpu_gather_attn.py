@@ -59,8 +59,27 @@ def run_attn(dtype, batch, Hq, Hkv, d, block, n_ctx, seed=0, seqs=None, paged=Fa
     bv = rnd((batch, block, Hkv, d))
     hd = H.heads(Hq, Hkv, d, dtype)
     lens = to_dev(n_ctx)
-    tq, tck, tcv, tbk, tbv = map(to_dev, (q, ck, cv, bk, bv))
-    ctx = H.kv_view(tck, tcv, lens, int(n_ctx.max()))
+    tq, tbk, tbv = map(to_dev, (q, bk, bv))
+    if paged:
+        # the same context rows in pages of `paged` rows, physical pages in a
+        # seeded order: pages [n_pages][Hkv][P][d], page_table [batch][max_pages]
+        P = int(paged)
+        max_pages = (cap + P - 1) // P
+        perm = rng.permutation(batch * max_pages).astype(np.int32)
+        pt = perm.reshape(batch, max_pages)
+        pk = np.zeros((batch * max_pages, Hkv, P, d), dtype=ck.dtype)
+        pv = np.zeros_like(pk)
+        for b in range(batch):
+            for j in range(max_pages):
+                rows = slice(j * P, min((j + 1) * P, cap))
+                n = rows.stop - rows.start
+                pk[pt[b, j], :, :n] = ck[b, :, rows]
+                pv[pt[b, j], :, :n] = cv[b, :, rows]
+        tpk, tpv, tpt = map(to_dev, (pk, pv, pt))
+        ctx = H.kv_view(tpk, tpv, lens, int(n_ctx.max()), page_table=tpt)
+    else:
+        tck, tcv = map(to_dev, (ck, cv))
+        ctx = H.kv_view(tck, tcv, lens, int(n_ctx.max()))
     out = torch.zeros_like(tq)
     ws = H.workspace(H.block_attn_workspace(hd, batch, block, int(n_ctx.max())), DEV)
     H.block_attn(hd, batch, block, tq, ctx, tbk, tbv, out, ws)
@@ -107,6 +126,16 @@ def test_attn_bf16_layer_32k_pool_shape():
     """The denoising step of the 8B-class 32K layer: 16 sequences, 1638 pool
     rows + 32 block rows per KV head; 4 sequences checked by the oracle."""
     run_attn("bf16", 16, 32, 8, 128, 32, [1638] * 16, seed=9, seqs=[0, 5, 10, 15])
+
+
+@pytest.mark.parametrize("dtype,d,P,n_ctx", [("bf16", 128, 16, [0, 1, 700, 5000]),
+                                             ("bf16", 64, 8, [33, 2048, 4100]),
+                                             ("f32", 64, 16, [17, 300, 1000])])
+def test_attn_paged_context(dtype, d, P, n_ctx):
+    """Context rows read through a page table (pages of P rows in a seeded
+    physical order), e.g. dense attention over a paged cache."""
+    run_attn(dtype, len(n_ctx), 16, 4, d, 32 if dtype == "bf16" else 4, n_ctx,
+             seed=P + d, paged=P)
 
 
 def test_attn_bf16_long_128k_pool_shape():
