@@ -127,6 +127,26 @@ __global__ __launch_bounds__(256) void repq_kernel(const void *__restrict__ q_se
 // half of the head dimension with the qbar half it holds in scalar registers.
 // The halves are added in a fixed order (low half + high half); the online
 // softmax statistics of the G heads are split between the two waves.
+// (chunk, KV head, sequence) of a workgroup of a (chunk, H_kv, batch) grid,
+// numbered chunk-major. Workgroups are dealt to the 8 XCDs round-robin by
+// linear id; numbered chunk-fastest, the low chunks that every sequence has
+// would all land on the same few XCDs when the sequences' lengths differ,
+// while with the chunk as the slowest index the (KV head, sequence) pairs
+// alternate over the XCDs and each gets an equal share of the valid chunks.
+struct ChunkOf {
+  int chunk, h, b;
+};
+__device__ __forceinline__ ChunkOf chunk_major() {
+  const int nbh = gridDim.y * gridDim.z;
+  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  ChunkOf c;
+  c.chunk = lin / nbh;
+  const int bhi = lin - c.chunk * nbh;
+  c.h = bhi % gridDim.y;
+  c.b = bhi / gridDim.y;
+  return c;
+}
+
 // Page numbers of the pages that hold rows [c0, c0 + kScoreChunk) of
 // sequence b, staged in LDS by the workgroup (paged views): a tile's page
 // lookup is then an LDS read instead of a global load that its row loads wait
@@ -168,7 +188,8 @@ __global__ __launch_bounds__(256, 4) void score_kernel(KvView kv,
   __shared__ double xch[2][2][64][GH];   // [pair][from half][row][g]
   __shared__ double red[4][GH], red2[4][GH];
 
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
@@ -358,7 +379,8 @@ __global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
   __shared__ __attribute__((aligned(16))) char lds[NW][WR * LSTR];
   __shared__ double red[NW][4], red2[NW][4];
 
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
@@ -497,7 +519,8 @@ __global__ __launch_bounds__(256) void norm_kernel(const int32_t *__restrict__ l
                                                    int64_t S_pad, int nslot, int64_t max_len) {
   __shared__ uint32_t sh_hist[kHistBins];
   __shared__ double sm[G], sinv[G];
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
@@ -790,7 +813,8 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(const int32_t *__restric
                                                         int64_t max_len) {
   __shared__ uint32_t sh_hist[kHistBins];
   __shared__ double sm[kMaxScoreRows], sinv[kMaxScoreRows];
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
@@ -879,7 +903,8 @@ __global__ __launch_bounds__(256) void out_kernel(KvView kv, const double *__res
   __shared__ double sm[kMaxScoreRows], sinv[kMaxScoreRows];
   __shared__ float wt[TR][NV];
   __shared__ float red[4][NV][D];
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
@@ -1238,7 +1263,8 @@ __global__ __launch_bounds__(256) void emit_count_kernel(
     const uint64_t *__restrict__ cut, uint32_t *__restrict__ ecnt, uint8_t *__restrict__ emark,
     int Hkv, int64_t S_pad, int nchunk, int64_t max_len) {
   __shared__ uint32_t wsum[4];
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t bh = (int64_t)b * Hkv + h;
   const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
@@ -1263,7 +1289,8 @@ __global__ __launch_bounds__(256) void emit_write_kernel(
     const uint8_t *__restrict__ emark, int32_t *__restrict__ idx_out, int Hkv, int nchunk,
     int64_t max_len) {
   __shared__ uint32_t wsum[4], wbase[4];
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const ChunkOf cid = chunk_major();
+  const int chunk = cid.chunk, h = cid.h, b = cid.b;
   const int64_t bh = (int64_t)b * Hkv + h;
   const int64_t S = min(max((int64_t)lens[b], (int64_t)0), max_len);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
