@@ -652,7 +652,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const double *__restrict__ qb
 // interleaved 16-row tiles with the next tile's loads in flight. Each cached
 // element is loaded and converted once per workgroup and feeds NG MFMAs (one
 // per group of 4 score rows). The score-row groups of one chunk have
-// consecutive block ids, so they read the chunk at about the same time.
+// consecutive linear ids, so they read the chunk at about the same time.
 template <int D, bool BF16, bool PAGED, int NG>
 __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
                                                             const double *__restrict__ qx,
@@ -674,7 +674,13 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
   __shared__ double qs[NS * 4 * NG * 4];
   __shared__ double red[NW][NQ], red2[NW][NQ];
 
-  const int vg = blockIdx.x % nvg, chunk = blockIdx.x / nvg, h = blockIdx.y, b = blockIdx.z;
+  // score-row group fastest, then (KV head, sequence), then chunk (see
+  // chunk_major)
+  const int nbh = gridDim.y * gridDim.z;
+  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int vg = lin % nvg, rest = lin / nvg;
+  const int chunk = rest / nbh, bhi = rest - chunk * nbh;
+  const int h = bhi % gridDim.y, b = bhi / gridDim.y;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
