@@ -137,13 +137,14 @@ struct ChunkOf {
   int chunk, h, b;
 };
 __device__ __forceinline__ ChunkOf chunk_major() {
-  const int nbh = gridDim.y * gridDim.z;
-  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int64_t nbh = (int64_t)gridDim.y * gridDim.z;
+  const int64_t lin =
+      blockIdx.x + (int64_t)gridDim.x * (blockIdx.y + (int64_t)gridDim.y * blockIdx.z);
   ChunkOf c;
-  c.chunk = lin / nbh;
-  const int bhi = lin - c.chunk * nbh;
-  c.h = bhi % gridDim.y;
-  c.b = bhi / gridDim.y;
+  c.chunk = (int)(lin / nbh);
+  const int bhi = (int)(lin - (int64_t)c.chunk * nbh);
+  c.h = bhi % (int)gridDim.y;
+  c.b = bhi / (int)gridDim.y;
   return c;
 }
 
@@ -676,11 +677,13 @@ __global__ __launch_bounds__(256, 2) void score_rows_kernel(KvView kv,
 
   // score-row group fastest, then (KV head, sequence), then chunk (see
   // chunk_major)
-  const int nbh = gridDim.y * gridDim.z;
-  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
-  const int vg = lin % nvg, rest = lin / nvg;
-  const int chunk = rest / nbh, bhi = rest - chunk * nbh;
-  const int h = bhi % gridDim.y, b = bhi / gridDim.y;
+  const int64_t nbh = (int64_t)gridDim.y * gridDim.z;
+  const int64_t lin =
+      blockIdx.x + (int64_t)gridDim.x * (blockIdx.y + (int64_t)gridDim.y * blockIdx.z);
+  const int vg = (int)(lin % nvg);
+  const int64_t rest = lin / nvg;
+  const int chunk = (int)(rest / nbh), bhi = (int)(rest - (int64_t)chunk * nbh);
+  const int h = bhi % (int)gridDim.y, b = bhi / (int)gridDim.y;
   const int64_t S = kv_len(kv, b);
   const int64_t c0 = (int64_t)chunk * kScoreChunk;
   if (c0 >= S) return;
