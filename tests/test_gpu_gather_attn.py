@@ -106,7 +106,8 @@ def test_attn_fp32_ragged(n_ctx):
 
 
 @pytest.mark.parametrize("G,block,d", [(4, 32, 128), (4, 16, 128), (4, 4, 128), (8, 32, 128),
-                                       (1, 32, 128), (2, 8, 64), (4, 32, 64), (1, 1, 64)])
+                                       (1, 32, 128), (2, 8, 64), (4, 32, 64), (1, 1, 64),
+                                       (4, 64, 128), (2, 64, 64), (8, 64, 128)])
 def test_attn_bf16_shapes(G, block, d):
     run_attn("bf16", 3, 2 * G, 2, d, block, [0, 97, 1300], seed=G * 100 + block + d)
 
