@@ -189,6 +189,17 @@ def test_select_xq_paged_ragged(x, page_size):
     assert check_select_xq(wl, x) == 0
 
 
+@pytest.mark.parametrize("G,x", [(4, 64), (8, 64), (8, 1)])
+def test_select_largest_block(G, x):
+    """Blocks of 64 rows (the largest): the mean over 64 query rows, and the
+    x-row selection up to every row of the block (x G = 512 score rows per KV
+    head, the largest the library takes)."""
+    wl = XQ.replace(name=f"B64 G{G} x{x}", block=64, num_q_heads=2 * G, seq_len=3000,
+                    seq_len_lo=700, seed=70 + G + x)
+    assert check_select(wl) == 0
+    assert check_select_xq(wl, x) == 0
+
+
 def test_select_xq_budget_edges_and_ties():
     inp = synth.make_host(XQ.replace(num_q_heads=8))
     wl = XQ.replace(num_q_heads=8)
