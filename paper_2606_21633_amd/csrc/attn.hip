@@ -476,14 +476,14 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
   }
 }
 
-// Merge of split-KV partials (log2-domain statistics), 4 outputs per thread.
+// Merge of split-KV partials (log2-domain statistics), 8 outputs per thread.
 __global__ __launch_bounds__(256) void attn_combine_kernel(
     const float *__restrict__ part_o, const float2 *__restrict__ part_ml,
     uint16_t *__restrict__ out, int block, int Hq, int Hkv, int G, int M, int D,
     int nsplit) {
   const int h = blockIdx.y, b = blockIdx.z;
   const int idx = blockIdx.x * 256 + threadIdx.x;
-  const int r = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
+  const int r = idx / (D / 8), d0 = (idx % (D / 8)) * 8;
   if (r >= M) return;
   const int64_t p0 = ((int64_t)b * Hkv + h) * nsplit;
   // part_ml holds (max * scale * log2(e), sum) per row and split. Splits are
@@ -499,32 +499,39 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(
 #pragma unroll
     for (int u = 0; u < GRP; ++u) mx = fmaxf(mx, ml[u].x);
   }
-  float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
+  float den = 0.f, n[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) n[e] = 0.f;
   for (int s0 = 0; s0 < nsplit; s0 += GRP) {
     float2 ml[GRP];
-    float4 v[GRP];
+    float4 v[GRP][2];
 #pragma unroll
     for (int u = 0; u < GRP; ++u) {
       const bool in = s0 + u < nsplit;
       const int64_t sp = p0 + (in ? s0 + u : 0);
       ml[u] = in ? part_ml[sp * M + r] : make_float2(-INFINITY, 0.f);
-      v[u] = *reinterpret_cast<const float4 *>(part_o + (sp * M + r) * D + d0);
+      const float4 *src = reinterpret_cast<const float4 *>(part_o + (sp * M + r) * D + d0);
+      v[u][0] = src[0];
+      v[u][1] = src[1];
     }
 #pragma unroll
     for (int u = 0; u < GRP; ++u) {
       if (ml[u].x == -INFINITY) continue;
       const float w = __builtin_amdgcn_exp2f(ml[u].x - mx);
       den += ml[u].y * w;
-      n0 += v[u].x * w; n1 += v[u].y * w; n2 += v[u].z * w; n3 += v[u].w * w;
+      n[0] += v[u][0].x * w; n[1] += v[u][0].y * w; n[2] += v[u][0].z * w; n[3] += v[u][0].w * w;
+      n[4] += v[u][1].x * w; n[5] += v[u][1].y * w; n[6] += v[u][1].z * w; n[7] += v[u][1].w * w;
     }
   }
   const float inv = 1.f / den;
   const int g = r / block, i = r % block;
   uint16_t *orow = out + (((int64_t)b * block + i) * Hq + h * G + g) * D + d0;
-  uint2 w;
-  w.x = pack2(n0 * inv, n1 * inv);
-  w.y = pack2(n2 * inv, n3 * inv);
-  *reinterpret_cast<uint2 *>(orow) = w;
+  uint4 w;
+  w.x = pack2(n[0] * inv, n[1] * inv);
+  w.y = pack2(n[2] * inv, n[3] * inv);
+  w.z = pack2(n[4] * inv, n[5] * inv);
+  w.w = pack2(n[6] * inv, n[7] * inv);
+  *reinterpret_cast<uint4 *>(orow) = w;
 }
 
 // fp32 path: one wave per query row; lanes split the keys of a 64-key pass,
@@ -708,7 +715,7 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, int g
   return hipErrorInvalidValue;
 #undef HERALD_ATTN
   if (p.nsplit > 1) {
-    const dim3 cg((p.M * (D / 4) + 255) / 256, Hkv, batch);
+    const dim3 cg((p.M * (D / 8) + 255) / 256, Hkv, batch);
     attn_combine_kernel<<<cg, 256, 0, stream>>>(part_o, part_ml, oo, block, Hq, Hkv, G,
                                                 p.M, D, p.nsplit);
   }
