@@ -77,12 +77,14 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // LDS bytes of attn_bf16_kernel: the K/V ring (P pipelines x 2 stages of a
-// 32-key K and V tile), or the pipeline merge area if that is larger.
+// 32-key K and V tile), or the pipeline merge area (the O blocks each wave
+// hands to other pipelines and its (max, sum) per lane) if that is larger.
 template <int D, int RW, int NWP, int P>
 constexpr int attn_smem_bytes() {
   constexpr int ring = P * 2 * 2 * 32 * (2 * D);
-  constexpr int slot = (RW / 16) * ((D / 16 + 1) * 4 + 1) + 1;
-  constexpr int merge = (P - 1) * NWP * 64 * slot * 4;
+  constexpr int merge =
+      P > 1 ? P * NWP * (RW / 16) * 64 * ((D / 16 - D / 16 / P) * 16 + 8) : 0;
+  static_assert(merge <= 160 * 1024, "merge area exceeds the LDS of a CU");
   return ring > merge ? ring : merge;
 }
 
@@ -412,66 +414,95 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
     round(it + 1, kr[0], vr[0]);
   }
 
-  // merge pipelines 1..P-1 into pipeline 0 through LDS (same rows and lanes)
+  // Merge of the P pipelines, spread over every wave: wave w of pipeline p
+  // merges d-blocks [p * SL, (p + 1) * SL) of its query rows over the P
+  // pipelines and writes them out. Its own share of those stays in
+  // registers; through LDS each wave hands the other pipelines their d-blocks
+  // ([pipeline][wave][cb][NX d-blocks][lane], 16 B each, the writer's own
+  // slice left out) and its (max, sum) ([pipeline][wave][cb][lane]).
+  constexpr int SL = NDB / P;   // d-blocks each wave merges and writes
+  constexpr int NX = NDB - SL;  // d-blocks each wave hands over
+  static_assert(SL * P == NDB, "d-blocks must split evenly over the pipelines");
+  const int db0 = pipe * SL;
+  f32x4 acc[CB][SL];
+  float mrow[CB], lrow[CB];
   if constexpr (P > 1) {
-    constexpr int SLOT = CB * ((NDB + 1) * 4 + 1) + 1;  // odd: no bank conflicts
-    float *xs = reinterpret_cast<float *>(smem);
-    if (pipe > 0) {
-      float *x = xs + ((size_t)((pipe - 1) * NWP + w) * 64 + lane) * SLOT;
+    f32x4 *xo = reinterpret_cast<f32x4 *>(smem);
+    float2 *xm = reinterpret_cast<float2 *>(smem + (size_t)P * NWP * CB * NX * 64 * 16);
+    const int pw = pipe * NWP + w;
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) {
+    for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
-        for (int db = 0; db <= NDB; ++db)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) x[cb * ((NDB + 1) * 4 + 1) + db * 4 + j] = o[cb][db][j];
-        x[cb * ((NDB + 1) * 4 + 1) + (NDB + 1) * 4] = m_run[cb];
+      for (int db = 0; db < NDB; ++db) {
+        const int q = db / SL;  // the pipeline that merges this d-block
+        if (q != pipe)
+          xo[((pw * CB + cb) * NX + db - (q > pipe ? SL : 0)) * 64 + lane] = o[cb][db];
       }
+      xm[(pw * CB + cb) * 64 + lane] = make_float2(m_run[cb], o[cb][NDB][0]);
     }
     lds_barrier();
-    if (pipe > 0) return;
-#pragma unroll 1
-    for (int pp = 1; pp < P; ++pp) {
-      const float *x = xs + ((size_t)((pp - 1) * NWP + w) * 64 + lane) * SLOT;
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) {
-        const float *xc = x + cb * ((NDB + 1) * 4 + 1);
-        const float m1 = xc[(NDB + 1) * 4];
-        const float mm = fmaxf(m_run[cb], m1);
-        const float a0 =
-            m_run[cb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run[cb] - mm) * sl2);
-        const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mm) * sl2);
+    for (int cb = 0; cb < CB; ++cb) {
+      float2 ml[P];
 #pragma unroll
-        for (int db = 0; db <= NDB; ++db)
+      for (int pp = 0; pp < P; ++pp) ml[pp] = xm[((pp * NWP + w) * CB + cb) * 64 + lane];
+      float mm = ml[0].x;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) o[cb][db][j] = o[cb][db][j] * a0 + xc[db * 4 + j] * a1;
-        m_run[cb] = mm;
+      for (int pp = 1; pp < P; ++pp) mm = fmaxf(mm, ml[pp].x);
+      float l = 0.f;
+#pragma unroll
+      for (int sb = 0; sb < SL; ++sb) acc[cb][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int pp = 0; pp < P; ++pp) {
+        // (a pipeline that saw only masked keys has max -inf and adds nothing)
+        const float sc =
+            ml[pp].x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((ml[pp].x - mm) * sl2);
+        l += sc * ml[pp].y;
+        if (pp == pipe) {
+#pragma unroll
+          for (int sb = 0; sb < SL; ++sb) acc[cb][sb] += sc * o[cb][pp * SL + sb];
+        } else {
+          const int pos = db0 - (pipe > pp ? SL : 0);  // where pipeline pp put them
+#pragma unroll
+          for (int sb = 0; sb < SL; ++sb)
+            acc[cb][sb] += sc * xo[(((pp * NWP + w) * CB + cb) * NX + pos + sb) * 64 + lane];
+        }
       }
+      mrow[cb] = mm;
+      lrow[cb] = l;
+    }
+  } else {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+#pragma unroll
+      for (int sb = 0; sb < SL; ++sb) acc[cb][sb] = o[cb][sb];
+      mrow[cb] = m_run[cb];
+      lrow[cb] = o[cb][NDB][0];
     }
   }
-  // lane holds d = 16 db + 4 q4 + j of query row rbase + 16 cb + l16
+  // lane holds d = 16 (db0 + sb) + 4 q4 + j of query row rbase + 16 cb + l16
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     if (!rvalid[cb]) continue;
     const int r = rbase + 16 * cb + l16;
-    const float l_run = o[cb][NDB][0];
     if (nsplit == 1) {
-      const float inv = 1.f / l_run;
-      uint16_t *orow = out + qoff[cb];
+      const float inv = 1.f / lrow[cb];
+      uint16_t *orow = out + qoff[cb] + 16 * db0 + 4 * q4;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
+      for (int sb = 0; sb < SL; ++sb) {
         uint2 wd;
-        wd.x = pack2(o[cb][db][0] * inv, o[cb][db][1] * inv);
-        wd.y = pack2(o[cb][db][2] * inv, o[cb][db][3] * inv);
-        *reinterpret_cast<uint2 *>(orow + 16 * db + 4 * q4) = wd;
+        wd.x = pack2(acc[cb][sb][0] * inv, acc[cb][sb][1] * inv);
+        wd.y = pack2(acc[cb][sb][2] * inv, acc[cb][sb][3] * inv);
+        *reinterpret_cast<uint2 *>(orow + 16 * sb) = wd;
       }
     } else {
       const int64_t pidx = ((int64_t)b * Hkv + h) * nsplit + split;
-      float *po = part_o + (pidx * M + r) * D;
+      float *po = part_o + (pidx * M + r) * D + 16 * db0 + 4 * q4;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-        *reinterpret_cast<float4 *>(po + 16 * db + 4 * q4) =
-            make_float4(o[cb][db][0], o[cb][db][1], o[cb][db][2], o[cb][db][3]);
-      if (q4 == 0) part_ml[pidx * M + r] = make_float2(m_run[cb] * sl2, l_run);
+      for (int sb = 0; sb < SL; ++sb)
+        *reinterpret_cast<float4 *>(po + 16 * sb) =
+            make_float4(acc[cb][sb][0], acc[cb][sb][1], acc[cb][sb][2], acc[cb][sb][3]);
+      if (pipe == 0 && q4 == 0) part_ml[pidx * M + r] = make_float2(mrow[cb] * sl2, lrow[cb]);
     }
   }
 }
