@@ -76,6 +76,9 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Most query groups that attn_bf16_kernel orders by context length.
+constexpr int kOrderMax = 256;
+
 // LDS bytes of attn_bf16_kernel: the K/V ring (P pipelines x 2 stages of a
 // 32-key K and V tile), or the pipeline merge area (the O blocks each wave
 // hands to other pipelines and its (max, sum) per lane) if that is larger.
@@ -106,7 +109,8 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
     const uint16_t *__restrict__ q, KvView ctx, const uint16_t *__restrict__ blk_k,
     const uint16_t *__restrict__ blk_v, uint16_t *__restrict__ out,
     float *__restrict__ part_o, float2 *__restrict__ part_ml, int block, int Hq, int Hkv,
-    int G, int M, int n_mblk, int nsplit, int keys_per_split, float sl2, int groups) {
+    int G, int M, int n_mblk, int nsplit, int keys_per_split, float sl2, int groups,
+    int order) {
   constexpr int KT = 32;             // keys per tile
   constexpr int CB = RW / 16;        // column blocks (16 query rows) per wave
   constexpr int NKS = D / 32;        // k-steps of K Q^T
@@ -142,7 +146,44 @@ __global__ __launch_bounds__(NWP * P * 64, 1) void attn_bf16_kernel(
     }
   }
   const int split = grp % nsplit;
-  const int h = (grp / nsplit) % Hkv, b = grp / nsplit / Hkv;
+  const int h = (grp / nsplit) % Hkv;
+  int b = grp / nsplit / Hkv;
+  if (order) {
+    // More workgroups than CUs: the later ones start as earlier ones finish,
+    // so b is taken as a rank and the query groups run longest context first
+    // (ties to the lower index), leaving the short ones for the end of the
+    // grid. Every thread takes part; the ranks are a permutation, so exactly
+    // one query group matches.
+    // (lengths padded with -1 to a multiple of 16, which rank below every
+    // length, so the rank loop reads 16 at a time without a bound check)
+    __shared__ __attribute__((aligned(16))) int lens_s[kOrderMax];
+    __shared__ int pick_s;
+    const int nb = gridDim.x / (n_mblk * nsplit * Hkv);
+    const int nb16 = (nb + 15) & ~15;
+    for (int j = threadIdx.x; j < nb16; j += blockDim.x)
+      lens_s[j] = j < nb ? (int)kv_len(ctx, j / groups) : -1;
+    __syncthreads();
+    for (int j = threadIdx.x; j < nb; j += blockDim.x) {
+      const int lj = lens_s[j];
+      int rank = 0;
+      for (int i0 = 0; i0 < nb16; i0 += 16) {
+        int4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const int4 *>(lens_s + i0 + 4 * u);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int i = i0 + 4 * u;
+          rank += (v[u].x > lj) | ((v[u].x == lj) & (i < j));
+          rank += (v[u].y > lj) | ((v[u].y == lj) & (i + 1 < j));
+          rank += (v[u].z > lj) | ((v[u].z == lj) & (i + 2 < j));
+          rank += (v[u].w > lj) | ((v[u].w == lj) & (i + 3 < j));
+        }
+      }
+      if (rank == b) pick_s = j;
+    }
+    __syncthreads();
+    b = pick_s;
+  }
   // b indexes the query groups (queries, block KV, outputs); groups of one
   // sequence share its context
   const int bc = b / groups;
@@ -722,6 +763,12 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, int g
   const uint16_t *bk = (const uint16_t *)blk_k, *bv = (const uint16_t *)blk_v;
   uint16_t *oo = (uint16_t *)out;
   const bool paged = ctx.pt != nullptr;
+  // Longest context first when the workgroups do not all fit at once and
+  // each covers enough keys (from 1024, tens of microseconds of work) that
+  // ranking the query groups (about a microsecond per workgroup) is small
+  // beside the idle tail of a ragged batch it removes.
+  const int order =
+      grid > kTargetWgs && batch > 1 && batch <= kOrderMax && max_ctx + block >= 1024;
 #define HERALD_ATTN(D_, RW_, NW_, P_, PG_)                                               \
   if (D == D_ && p.rows_per_wave == RW_ && p.nwaves == NW_ && p.pipes == P_ &&            \
       paged == PG_) {                                                                    \
@@ -733,7 +780,8 @@ hipError_t launch_block_attn(const herald_heads &hd, int batch, int block, int g
     if (attr_err != hipSuccess) return attr_err;                                         \
     kfn<<<grid, NW_ * P_ * 64, kSmem, stream>>>(qq, ctx, bk, bv, oo, part_o, part_ml,     \
                                                block, Hq, Hkv, G, p.M, p.n_mblk,         \
-                                               p.nsplit, p.keys_per_split, sl2, groups); \
+                                               p.nsplit, p.keys_per_split, sl2, groups,  \
+                                               order);                                   \
   } else
   HERALD_ATTN(64, 32, 2, 4, false) HERALD_ATTN(64, 32, 1, 4, false)
   HERALD_ATTN(64, 16, 1, 4, false) HERALD_ATTN(64, 32, 4, 2, false)

@@ -117,6 +117,18 @@ def test_attn_bf16_ragged_tiles(n_ctx):
     run_attn("bf16", len(n_ctx), 32, 8, 128, 32, n_ctx, seed=len(n_ctx))
 
 
+@pytest.mark.parametrize("block,paged", [(32, False), (16, 16)])
+def test_attn_bf16_ragged_more_groups_than_cus(block, paged):
+    """40 sequences of seeded ragged lengths (equal lengths and empty contexts
+    among them): more workgroups than CUs, so the kernel takes the sequences
+    longest context first; every output must still land on its own sequence."""
+    rng = np.random.default_rng(41)
+    n_ctx = rng.integers(0, 3000, size=40)
+    n_ctx[[3, 17]] = 0
+    n_ctx[[5, 6, 30]] = 1234
+    run_attn("bf16", 40, 32, 8, 128, block, n_ctx.tolist(), seed=42, paged=paged)
+
+
 def test_attn_bf16_many_key_splits():
     """One sequence and one KV head over 20000 context rows: the plan splits
     the keys 128 ways, so the combine merges its partials in 16 groups."""
