@@ -207,6 +207,18 @@ def test_attn_groups_share_the_context_not_each_other(dtype, groups, block, n_ct
     run_attn_groups(dtype, len(n_ctx), groups, 8, 2, d, block, n_ctx, seed=groups * 10 + block)
 
 
+def test_attn_groups_ragged_more_groups_than_cus():
+    """24 sequences of ragged lengths, 2 query groups each (48 query groups
+    over 8 KV heads, two row blocks each): the kernel runs the query groups
+    longest context first, each group still attending to its own sequence's
+    context and its own block rows."""
+    rng = np.random.default_rng(43)
+    n_ctx = rng.integers(0, 2500, size=24)
+    n_ctx[[2, 11]] = 0
+    n_ctx[[4, 5]] = 1500
+    run_attn_groups("bf16", 24, 2, 32, 8, 128, 32, n_ctx.tolist(), seed=44)
+
+
 def test_attn_groups_layer_32k_draft_step_shape():
     """The 2B-token step of the 8B-class layer: denoising and draft groups of
     32 queries over the 1638-row pool; 3 sequences checked by the oracle."""
