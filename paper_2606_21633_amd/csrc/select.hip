@@ -392,14 +392,16 @@ __global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
   const int g = lane & 3;                                 // head (B column, result)
   const int zrow = 4 * ((lane >> 2) & 3) + (lane >> 4);   // result row within 16
 
-  // B operand of every step: qbar at the permuted element, zero past G
-  double bq[NS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const int e = (s / EPP) * (4 * EPP) + kq * EPP + s % EPP;
-    const double q = qbar[(bh * D + e) * G + (g < G ? g : G - 1)];
-    bq[s] = g < G ? q : 0.0;
+  // B operand of every step: qbar at the permuted element, zero past G,
+  // in LDS as [step][slot kq][head g] (the lanes of one (kq, g) share it)
+  __shared__ double bqs[NS * 16];
+  for (int i = threadIdx.x; i < NS * 16; i += 256) {
+    const int s = i >> 4, kk = (i >> 2) & 3, gg = i & 3;
+    const int e = (s / EPP) * (4 * EPP) + kk * EPP + s % EPP;
+    bqs[i] = gg < G ? qbar[(bh * D + e) * G + gg] : 0.0;
   }
+  __syncthreads();
+  const double *bql = bqs + kq * 4 + g;
 
   const int lr = lane / LPR, lc = lane % LPR;
   const char *kbase = kv.k + ((int64_t)b * kv.sb + (int64_t)h * kv.sh) * ELT + lc * 16;
@@ -472,7 +474,8 @@ __global__ __launch_bounds__(256, 2) void score_mfma_kernel(KvView kv,
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
           acc[c][hh] = __builtin_amdgcn_mfma_f64_4x4x4f64(elem(a[c], s + hh * NH),
-                                                          bq[s + hh * NH], acc[c][hh], 0, 0, 0);
+                                                          bql[(s + hh * NH) * 16], acc[c][hh],
+                                                          0, 0, 0);
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int64_t s = r0 + 16 * c + zrow;
