@@ -129,6 +129,15 @@ def test_attn_bf16_ragged_more_groups_than_cus(block, paged):
     run_attn("bf16", 40, 32, 8, 128, block, n_ctx.tolist(), seed=42, paged=paged)
 
 
+def test_attn_bf16_ragged_most_ordered_groups():
+    """256 sequences, the most the kernel orders by context length (its LDS
+    table of lengths full), ragged contexts up to 1200 rows."""
+    rng = np.random.default_rng(45)
+    n_ctx = rng.integers(0, 1200, size=256)
+    n_ctx[[0, 255]] = 1199
+    run_attn("bf16", 256, 8, 2, 128, 16, n_ctx.tolist(), seed=46)
+
+
 def test_attn_bf16_many_key_splits():
     """One sequence and one KV head over 20000 context rows: the plan splits
     the keys 128 ways, so the combine merges its partials in 16 groups."""
