@@ -67,6 +67,8 @@ def parse():
                     help="attention steps per sampled sequence (0: all T)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB MiB (counter calibration)")
+    ap.add_argument("--read-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain read (sum) of MIB MiB (counter calibration)")
     return ap.parse_args()
 
 
@@ -87,6 +89,8 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.read_calibration:
+        return read_calibration(args.read_calibration)
     if args.workload == "ragged":
         return bench_ragged(args)
     if args.workload == "pipeline36":
@@ -373,6 +377,19 @@ def copy_calibration(mib: int):
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration": True, "bytes_read_per_launch": n * 4,
                       "bytes_written_per_launch": n * 4, "launches": 5}), flush=True)
+
+
+def read_calibration(mib: int):
+    """A plain streaming read of known size (a sum over fp32, 5 times): the
+    FETCH_SIZE of a kernel that only reads, beside the copy's."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    for _ in range(5):
+        src.sum()
+    torch.cuda.synchronize()
+    print(json.dumps({"read_calibration": True, "bytes_read_per_launch": n * 4,
+                      "launches": 5}), flush=True)
 
 
 def _timed(fn, reps, stream):

@@ -7,11 +7,14 @@
         events, followed by M launches timed one by one).
 
     python -m paper_2606_21633_amd.profsum traffic --fetch DIR --write DIR
-            --copy-fetch DIR --copy-write DIR --copy-bytes B --kernel NAME
-            --last N --source-sha256 HEX
+            --copy-fetch DIR --copy-write DIR --copy-bytes B [--read-fetch DIR]
+            --kernel NAME --last N --source-sha256 HEX
         FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the kernel's last N
         dispatches, each scaled by bytes / counter of a plain copy of B bytes
-        read and B written, and the resulting HBM bytes per launch.
+        read and B written, and the resulting HBM bytes per launch. With
+        --read-fetch, FETCH_SIZE is scaled by that of a plain read of B bytes
+        instead (a kernel that reads and hardly writes counts its reads like
+        the read, not like the copy).
 
 Only reads CSV files; nothing here touches the GPU.
 """
@@ -94,15 +97,22 @@ def traffic(args) -> None:
     w_kib, nw = _counter(args.write, "WRITE_SIZE", args.kernel, args.last, args.skip_last)
     cf_kib, _ = _counter(args.copy_fetch, "FETCH_SIZE", args.copy_kernel, 0)
     cw_kib, _ = _counter(args.copy_write, "WRITE_SIZE", args.copy_kernel, 0)
-    sf = args.copy_bytes / (cf_kib * 1024.0)
+    sfc = args.copy_bytes / (cf_kib * 1024.0)
     sw = args.copy_bytes / (cw_kib * 1024.0)
+    sf = sfc
     fetch_b = f_kib * 1024.0 * sf
     write_b = w_kib * 1024.0 * sw
     print(f"{args.kernel}: FETCH_SIZE {f_kib:.1f} KiB/dispatch ({nf} dispatches), "
           f"WRITE_SIZE {w_kib:.1f} KiB/dispatch ({nw} dispatches)")
     print(f"copy calibration ({args.copy_kernel}, {args.copy_bytes} B read and written): "
-          f"FETCH_SIZE {cf_kib:.1f} KiB -> factor {sf:.4f}; WRITE_SIZE {cw_kib:.1f} KiB -> "
+          f"FETCH_SIZE {cf_kib:.1f} KiB -> factor {sfc:.4f}; WRITE_SIZE {cw_kib:.1f} KiB -> "
           f"factor {sw:.4f}")
+    if args.read_fetch:
+        rf_kib, _ = _counter(args.read_fetch, "FETCH_SIZE", args.read_kernel, 0)
+        sf = args.copy_bytes / (rf_kib * 1024.0)
+        print(f"read calibration ({args.read_kernel}, {args.copy_bytes} B read): FETCH_SIZE "
+              f"{rf_kib:.1f} KiB -> factor {sf:.4f}, used for FETCH_SIZE")
+        fetch_b = f_kib * 1024.0 * sf
     print(f"HBM bytes per launch: fetch {fetch_b:.0f} + write {write_b:.0f} = "
           f"{fetch_b + write_b:.0f}")
     print(f"traffic: source_sha256={args.source_sha256} bytes_per_launch={fetch_b + write_b:.0f} "
@@ -122,6 +132,8 @@ def main(argv=None) -> None:
         c.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     c.add_argument("--copy-bytes", type=float, required=True)
     c.add_argument("--copy-kernel", default="vectorized_elementwise_kernel")
+    c.add_argument("--read-fetch", default="")
+    c.add_argument("--read-kernel", default="reduce_kernel")
     c.add_argument("--kernel", required=True)
     c.add_argument("--last", type=int, default=0)
     c.add_argument("--skip-last", type=int, default=0)

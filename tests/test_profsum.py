@@ -66,6 +66,25 @@ def test_traffic_scales_each_counter_by_its_copy_calibration(tmp_path, capsys):
     assert float(kv["bytes_per_launch"]) == pytest.approx(2 * 1000.0 * 1024 + 40.0 * 1024)
 
 
+def test_traffic_scales_fetch_by_the_read_calibration_when_given(tmp_path, capsys):
+    gib = 1 << 30
+    red = "void at::native::reduce_kernel<512, 1, op>(args)"
+    _counters(str(tmp_path / "f"), "FETCH_SIZE", [(ATTN, 1000.0)])
+    _counters(str(tmp_path / "w"), "WRITE_SIZE", [(ATTN, 40.0)])
+    _counters(str(tmp_path / "cf"), "FETCH_SIZE", [(COPY, gib / 1024 / 2.4)])
+    _counters(str(tmp_path / "cw"), "WRITE_SIZE", [(COPY, gib / 1024)])
+    # the plain read counts 1/2 of its bytes; the copy 1/2.4 of its reads
+    _counters(str(tmp_path / "rf"), "FETCH_SIZE", [(red, gib / 1024 / 2)])
+    profsum.main(["traffic", "--fetch", str(tmp_path / "f"), "--write", str(tmp_path / "w"),
+                  "--copy-fetch", str(tmp_path / "cf"), "--copy-write", str(tmp_path / "cw"),
+                  "--read-fetch", str(tmp_path / "rf"), "--copy-bytes", str(gib),
+                  "--kernel", "attn_bf16_kernel"])
+    line = [x for x in capsys.readouterr().out.splitlines() if x.startswith("traffic:")][0]
+    kv = dict(tok.split("=") for tok in line.split()[1:])
+    assert float(kv["fetch"]) == pytest.approx(2 * 1000.0 * 1024)
+    assert float(kv["write"]) == pytest.approx(40.0 * 1024)
+
+
 def test_bench_reports_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     import bench
     from paper_2606_21633_amd import synth
